@@ -1,0 +1,230 @@
+"""Seeded synthetic workloads for chunked verification attention.
+
+This module only draws inputs: lengths, and q / k / v values.  It holds none of
+the attention arithmetic, so both the HIP path and the fp64 CPU oracle can take
+their inputs from it without sharing any code of the method.
+
+Shapes follow the paper's problem statement for the chunked-attention operator
+(Section 5.1, "Chunked Attention"): per sequence, n draft tokens (the chunk)
+attend to l cached tokens plus the chunk itself.  The KV cache is the paper's
+4-D [b, h, s, d] tensor (Section 5.2, CPU/GPU separation), here
+[B, Hkv, S_max, D]; rows [0, l_b) hold the cached context and rows
+[l_b, l_b + c_b) the chunk's own K/V, already appended.  Queries are
+token-major [B, C_max, Hq, D].
+
+The five workloads stand in for the paper's APPS and CNN/DailyMail runs of
+Mixtral-8x7B (Section 6.1, dataset table): those datasets and model weights are
+not used; lengths are drawn from distributions that cover their prefix lengths
+(APPS mean 566 input tokens plus up to 1024 generated; CNN/DM mean 1006), and
+Mixtral's attention shape (32 query heads, 8 KV heads, head_dim 128) is used.
+
+Recipe (all draws with numpy's PCG64 ``default_rng``):
+  * lengths: ``default_rng(seed)``; context lengths first, then chunk lengths.
+    Uniform integer ranges are inclusive.  Log-uniform is
+    ``floor(exp(U(ln lo, ln hi)))``.
+  * q: ``default_rng([seed, 0])``, N(0, 1) float32 of shape [B, C_max, Hq, D].
+  * k slab of sequence b: ``default_rng([seed, 1, b])``, N(0, 1) float32 of
+    shape [Hkv, T_b, D] written to rows [0, T_b); v likewise with
+    ``[seed, 2, b]``.  Each sequence's slab can therefore be regenerated on its
+    own, which lets a test check sampled sequences of a large workload.
+  * bf16 workloads round each float32 value once, to nearest-even, to bf16; the
+    same bits feed the GPU and the oracle.
+  * Rows that hold no valid data (cache rows >= T_b, query rows >= c_b) are
+    filled with ``fill`` (NaN by default) so that any read of them shows up.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Optional, Sequence
+
+import numpy as np
+
+BF16_NAN = np.uint16(0x7FC0)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    index: int            # 1-based; also the RNG seed
+    B: int
+    Hq: int
+    Hkv: int
+    D: int
+    dtype: str            # "f32" or "bf16"
+    ctx: tuple            # ("fixed", [..]) | ("uniform", lo, hi) | ("loguniform", lo, hi)
+    chunk: tuple          # ("fixed", n) | ("uniform", lo, hi)
+    description: str
+
+    @property
+    def group(self) -> int:
+        return self.Hq // self.Hkv
+
+    @property
+    def C_max(self) -> int:
+        kind = self.chunk[0]
+        return self.chunk[1] if kind == "fixed" else self.chunk[2]
+
+    @property
+    def ctx_hi(self) -> int:
+        kind = self.ctx[0]
+        return max(self.ctx[1]) if kind == "fixed" else self.ctx[2]
+
+    @property
+    def S_max(self) -> int:
+        return round_up(self.ctx_hi + self.C_max, 256)
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.D)
+
+    @property
+    def elt_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+
+def round_up(x: int, m: int) -> int:
+    return (x + m - 1) // m * m
+
+
+WORKLOADS = [
+    Workload("tiny_fp32", 1, B=2, Hq=4, Hkv=1, D=64, dtype="f32",
+             ctx=("fixed", [128, 200]), chunk=("fixed", 4),
+             description="tiny fp32: B=2, Hq=4, Hkv=1, D=64, ctx 128/200, chunk 4"),
+    Workload("mixtral_b64", 2, B=64, Hq=32, Hkv=8, D=128, dtype="bf16",
+             ctx=("uniform", 512, 2048), chunk=("fixed", 5),
+             description="Mixtral-8x7B attention shape, bf16: B=64, Hq=32, Hkv=8, D=128, "
+                         "ctx U[512,2048], chunk 5"),
+    Workload("large_batch_b256", 3, B=256, Hq=32, Hkv=8, D=128, dtype="bf16",
+             ctx=("uniform", 1024, 4096), chunk=("fixed", 8),
+             description="large batch, bf16: B=256, Hq=32, Hkv=8, D=128, ctx U[1024,4096], chunk 8"),
+    Workload("long_ctx_b32", 4, B=32, Hq=32, Hkv=8, D=128, dtype="bf16",
+             ctx=("loguniform", 16384, 32768), chunk=("fixed", 4),
+             description="long ragged contexts, bf16: B=32, Hq=32, Hkv=8, D=128, "
+                         "ctx logU[16384,32768], chunk 4"),
+    Workload("ragged_chunk_b128", 5, B=128, Hq=28, Hkv=4, D=128, dtype="bf16",
+             ctx=("uniform", 256, 4096), chunk=("uniform", 1, 16),
+             description="ragged chunks, wide GQA, bf16: B=128, Hq=28, Hkv=4, D=128, "
+                         "ctx U[256,4096], chunk U[1,16]"),
+]
+BY_NAME = {w.name: w for w in WORKLOADS}
+
+
+def get(name_or_index) -> Workload:
+    if isinstance(name_or_index, int):
+        return WORKLOADS[name_or_index - 1]
+    return BY_NAME[name_or_index]
+
+
+def draw_lengths(w: Workload):
+    """Context and chunk lengths (int32 [B] each) of workload ``w``."""
+    rng = np.random.default_rng(w.index)
+    kind = w.ctx[0]
+    if kind == "fixed":
+        ctx = np.asarray(w.ctx[1], dtype=np.int64)
+    elif kind == "uniform":
+        ctx = rng.integers(w.ctx[1], w.ctx[2] + 1, size=w.B)
+    elif kind == "loguniform":
+        u = rng.uniform(math.log(w.ctx[1]), math.log(w.ctx[2]), size=w.B)
+        ctx = np.floor(np.exp(u)).astype(np.int64)
+        ctx = np.clip(ctx, w.ctx[1], w.ctx[2])
+    else:
+        raise ValueError(kind)
+    kind = w.chunk[0]
+    if kind == "fixed":
+        chunk = np.full(w.B, w.chunk[1], dtype=np.int64)
+    elif kind == "uniform":
+        chunk = rng.integers(w.chunk[1], w.chunk[2] + 1, size=w.B)
+    else:
+        raise ValueError(kind)
+    return ctx.astype(np.int32), chunk.astype(np.int32)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bf16 (nearest, ties to even); returns the uint16 bits.
+
+    Input preparation only: the values are finite N(0, 1) draws or NaN fill.
+    """
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    u = x.view(np.uint32).astype(np.uint64)
+    rounded = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        rounded[nan] = BF16_NAN
+    return rounded
+
+
+def _encode(x: np.ndarray, dtype: str) -> np.ndarray:
+    return f32_to_bf16_bits(x) if dtype == "bf16" else np.ascontiguousarray(x, np.float32)
+
+
+def _fill_value(dtype: str, fill: float):
+    if dtype == "bf16":
+        return BF16_NAN if math.isnan(fill) else f32_to_bf16_bits(np.float32([fill]))[0]
+    return np.float32(fill)
+
+
+def kv_slab(w: Workload, b: int, T_b: int, which: str) -> np.ndarray:
+    """N(0,1) K or V rows [Hkv, T_b, D] of sequence ``b`` (encoded dtype)."""
+    stream = {"k": 1, "v": 2}[which]
+    rng = np.random.default_rng([w.index, stream, b])
+    x = rng.standard_normal((w.Hkv, T_b, w.D), dtype=np.float32)
+    return _encode(x, w.dtype)
+
+
+def make_inputs(w: Workload, fill: float = float("nan"),
+                batches: Optional[Sequence[int]] = None,
+                ctx_lens=None, chunk_lens=None):
+    """Materialise workload ``w`` on the host.
+
+    Returns a dict with q [B, C_max, Hq, D], k_cache / v_cache
+    [B, Hkv, S_max, D] (uint16 bf16 bits, or float32), ctx_lens, chunk_lens
+    (int32 [B]), scale, and the workload itself.  ``batches`` restricts the
+    cache fill to those sequences (others keep ``fill``), for sampled checks of
+    large workloads.  ``ctx_lens`` / ``chunk_lens`` override the drawn lengths.
+    """
+    ctx, chunk = draw_lengths(w)
+    if ctx_lens is not None:
+        ctx = np.asarray(ctx_lens, dtype=np.int32)
+    if chunk_lens is not None:
+        chunk = np.asarray(chunk_lens, dtype=np.int32)
+    B, C, S = len(ctx), w.C_max, w.S_max
+    fv = _fill_value(w.dtype, fill)
+    store = np.uint16 if w.dtype == "bf16" else np.float32
+
+    qrng = np.random.default_rng([w.index, 0])
+    q = _encode(qrng.standard_normal((B, C, w.Hq, w.D), dtype=np.float32), w.dtype)
+    for b in range(B):
+        q[b, chunk[b]:] = fv
+
+    k = np.full((B, w.Hkv, S, w.D), fv, dtype=store)
+    v = np.full((B, w.Hkv, S, w.D), fv, dtype=store)
+    todo = range(B) if batches is None else batches
+    for b in todo:
+        T_b = int(ctx[b]) + int(chunk[b])
+        k[b, :, :T_b] = kv_slab(w, b, T_b, "k")
+        v[b, :, :T_b] = kv_slab(w, b, T_b, "v")
+    return dict(q=q, k_cache=k, v_cache=v, ctx_lens=ctx, chunk_lens=chunk,
+                scale=w.scale, workload=w)
+
+
+def algorithmic_kv_bytes(w: Workload, ctx_lens, chunk_lens) -> int:
+    """K+V bytes of valid rows: sum_b Hkv * (l_b + c_b) * D * elt * 2.
+
+    This is the attention row of the paper's cost table (Section 3.2): memory
+    access 2*b*s*h/g elements, with h/g = Hkv*D the KV width per token, at the
+    workload's element size, and s = l_b + c_b per sequence.
+    """
+    T = np.asarray(ctx_lens, np.int64) + np.asarray(chunk_lens, np.int64)
+    return int(T.sum()) * w.Hkv * w.D * w.elt_bytes * 2
+
+
+def useful_flops(w: Workload, ctx_lens, chunk_lens) -> int:
+    """4 * sum_b c_b * g * Hkv * T_b * D: QK^T plus PV over all visible pairs.
+
+    Counts every (row, key) pair up to T_b; the causal mask inside the chunk
+    removes c*(c-1)/2 pairs per head, which this upper estimate keeps.
+    """
+    c = np.asarray(chunk_lens, np.int64)
+    T = np.asarray(ctx_lens, np.int64) + c
+    return int((c * T).sum()) * w.Hq * w.D * 4
