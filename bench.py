@@ -1,0 +1,226 @@
+"""Benchmark: chunked verification attention on one MI355X.
+
+One step = one call of the whole hot path (main split-KV kernel + combine
+kernel) over one batch of the synthetic workload, with every input already
+resident in HBM.  Prints ONE JSON line on stdout; progress goes to stderr.
+
+    python bench.py [--steps K] [--warmup W] [--workload mixtral_b64]
+
+value = effective KV GB/s = sum_b Hkv*(l_b + c_b)*D*elt*2 / t_step, the K+V
+bytes of every valid row (the attention row of the paper's cost table,
+2*b*s*h/g elements, Section 3.2).  Input sets are rotated so that successive
+steps read different HBM addresses and the KV cannot be served from the
+256 MB Infinity Cache.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "effective KV HBM GB/s and verified draft tokens/sec, Mixtral shape B=64"
+HBM_PEAK_GBS = 8000.0
+MAIN_KERNEL = "verify_main_kernel"
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2508_21706_amd", "csrc", "verify_attn.hip")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_digest() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """HBM bytes per launch of the main kernel from the committed rocprofv3
+    counter summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{MAIN_KERNEL}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_source_sha256_16") != source_digest():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(inp, w, budget_s: float):
+    """The fp64 oracle, timed on the host cores over a bounded sample of the
+    same workload: whole sequences, in order, until ~budget_s of work."""
+    from oracle import verify_attn_ref
+    from paper_2508_21706_amd import workloads as wl
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = 1
+    done = []
+    t_total = 0.0
+    for b in range(w.B):
+        units = [(b, h) for h in range(w.Hkv)]
+        t0 = time.perf_counter()
+        verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], inp["ctx_lens"], inp["chunk_lens"],
+                        w.scale, w.dtype, units=units)
+        t_total += time.perf_counter() - t0
+        done.append(b)
+        if t_total >= budget_s:
+            break
+    ctx = inp["ctx_lens"][done]
+    chunk = inp["chunk_lens"][done]
+    kv = wl.algorithmic_kv_bytes(w, ctx, chunk)
+    return {
+        "value": kv / t_total / 1e9,
+        "unit": "GB/s",
+        "cores": int(blas_threads),
+        "kind": "oracle",
+        "sample": f"{len(done)} of {w.B} sequences (all KV heads) of {w.name}, fp64 numpy oracle, "
+                  f"{t_total:.1f} s; {int(chunk.sum())} draft tokens -> "
+                  f"{chunk.sum() / t_total:.1f} verified tokens/s",
+        "host": {"os_cpu_count": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
+                 "cpu": platform.processor() or platform.machine()},
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mixtral_b64")
+    ap.add_argument("--split-len", type=int, default=0)
+    ap.add_argument("--rotate", type=int, default=0, help="input sets (0: enough for >= 1 GB)")
+    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work; 0 skips")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the verification-attention path has no "
+              "multi-GPU component in this build (see the sharding notes in the design doc).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2508_21706_amd as pkg
+    from paper_2508_21706_amd import workloads as wl
+
+    w = wl.get(args.workload)
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    inp = wl.make_inputs(w)
+    log(f"inputs for {w.name} drawn in {time.time() - t0:.1f} s")
+    ctx, chunk = inp["ctx_lens"], inp["chunk_lens"]
+    kv_bytes = wl.algorithmic_kv_bytes(w, ctx, chunk)
+    tokens = int(chunk.sum())
+    g = w.group
+    elt = w.elt_bytes
+    # algorithmic bytes of one main-kernel launch: K+V of valid rows, the valid
+    # query rows, and the fp32 out + lse rows it produces
+    launch_bytes = kv_bytes + int(chunk.sum()) * w.Hq * (w.D * elt + (w.D + 1) * 4)
+
+    def to_dev(a):
+        if w.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    set_bytes = inp["k_cache"].nbytes * 2
+    n_sets = args.rotate or max(4, int(np.ceil(1.0e9 / set_bytes)))
+    q = to_dev(inp["q"])
+    k0, v0 = to_dev(inp["k_cache"]), to_dev(inp["v_cache"])
+    sets = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_sets - 1)]
+    ctx_d = torch.from_numpy(ctx).to(dev)
+    chunk_d = torch.from_numpy(chunk).to(dev)
+    desc = pkg.desc_for(q, k0, args.split_len)
+    L = pkg.split_len(desc)
+    ws = pkg.alloc_workspace(desc, dev)
+    out = torch.empty((w.B, w.C_max, w.Hq, w.D), dtype=torch.float32, device=dev)
+    lse = torch.empty((w.B, w.C_max, w.Hq), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    log(f"{n_sets} input sets x {set_bytes / 1e6:.0f} MB, split_len={L}, "
+        f"KV bytes/step={kv_bytes / 1e6:.1f} MB, draft tokens/step={tokens}")
+
+    def step(i, events=None):
+        k, v = sets[i % n_sets]
+        pkg.verify_attn(q, k, v, ctx_d, chunk_d, w.scale, out=out, lse=lse, workspace=ws,
+                        split_len=args.split_len, stream=stream, events=events)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # timed region: exactly K steps, bracketed by synchronisations
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+
+    # main-kernel duration, from HIP events the library records on the same
+    # stream right before and after that kernel's launch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:          # materialise the HIP events
+        a.record(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(ev):
+        step(i, events=(a.cuda_event, b.cuda_event))
+    torch.cuda.synchronize()
+    main_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    main_avg_ms = float(main_ms.mean())
+
+    t = ms_per_step / 1e3
+    value = kv_bytes / t / 1e9
+    achieved = launch_bytes / (main_avg_ms / 1e3) / 1e9
+    traffic = load_traffic(w.name)
+    log(f"step {ms_per_step * 1e3:.1f} us -> {value:.0f} GB/s effective KV, {tokens / t / 1e6:.2f} M tok/s; "
+        f"main kernel avg {main_avg_ms * 1e3:.1f} us (p10 {np.percentile(main_ms, 10) * 1e3:.1f}, "
+        f"p90 {np.percentile(main_ms, 90) * 1e3:.1f}) -> {achieved:.0f} GB/s")
+
+    cpu = None
+    if args.cpu_budget > 0:
+        log("timing the fp64 oracle on the host ...")
+        cpu = cpu_baseline(inp, w, args.cpu_budget)
+
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
+                   "head_dim": w.D, "ctx_lens_sum": int(ctx.sum()), "chunk_lens_sum": tokens,
+                   "C_max": w.C_max, "S_max": w.S_max, "split_len": L, "input_sets": n_sets,
+                   "parallelism": "single GPU"},
+        "verified_tokens_per_s": round(tokens / t, 1),
+        "kv_bytes_per_step": kv_bytes,
+        "roofline": {"bound": "hbm", "kernel": MAIN_KERNEL, "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "algorithmic_bytes_per_launch": launch_bytes,
+                     "avg_launch_us": round(main_avg_ms * 1e3, 3)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,139 @@
+/*
+ * specmoe_verify.h -- chunked verification attention on MI355X (gfx950).
+ *
+ * The operation is the chunked-attention operator of speculative-decoding
+ * verification (SpecMoEOff, Section 5.1 "Chunked Attention in Target Model
+ * Verification"): for every sequence b, the n = c_b draft tokens of its chunk
+ * attend to the l = l_b cached tokens of its KV cache plus the chunk's own
+ * tokens.  With Q in R^{n x d}, K, V in R^{(l+n) x d} and the additive mask
+ * M in {-inf, 0}^{n x (l+n)} (draft token i sees every cached token and draft
+ * tokens 0..i, i.e. key positions j <= l + i):
+ *
+ *     out = softmax(scale * Q K^T + M) V,   lse = log sum_j exp(scale q.k_j + M_ij)
+ *
+ * per query head, with grouped-query attention: g = Hq / Hkv query heads share
+ * one KV head and query head h reads KV head h / g (the paper's group factor g,
+ * Section 3.1 "Model").  The KV cache is the paper's 4-D [b, h, s, d] layout
+ * (Section 5.2, "CPU/GPU separation for Draft Model Execution").
+ *
+ * All functions are plain C; every pointer named "device" is a HIP device
+ * pointer, every other pointer is a host pointer.
+ */
+#ifndef SPECMOE_VERIFY_H
+#define SPECMOE_VERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Element type of q, k_cache and v_cache.  out and lse are always float32. */
+typedef enum {
+  SPECMOE_F32 = 0,
+  SPECMOE_BF16 = 1
+} specmoe_dtype;
+
+/* Status codes returned by specmoe_verify_attn (0 = success). */
+enum {
+  SPECMOE_OK = 0,
+  SPECMOE_ERR_NULL_POINTER = -1,  /* a required pointer (or the descriptor) is NULL   */
+  SPECMOE_ERR_SHAPE = -2,         /* B < 0, Hq/Hkv <= 0, C_max < 1, S_max < C_max, or
+                                     sizes too large for the index arithmetic         */
+  SPECMOE_ERR_GQA = -3,           /* Hq is not a multiple of Hkv                      */
+  SPECMOE_ERR_HEAD_DIM = -4,      /* D is not 64 or 128                               */
+  SPECMOE_ERR_DTYPE = -5,         /* dtype is not a specmoe_dtype value               */
+  SPECMOE_ERR_ROWS = -6,          /* C_max * (Hq / Hkv) > 128 query rows per KV head  */
+  SPECMOE_ERR_SPLIT = -7,         /* split_len is not 0 and not a positive multiple of
+                                     the key tile, or it is smaller than C_max        */
+  SPECMOE_ERR_WORKSPACE = -8,     /* workspace smaller than the size query returns    */
+  SPECMOE_ERR_ALIGN = -9,         /* q, k_cache, v_cache, out or workspace is not
+                                     16-byte aligned                                  */
+  SPECMOE_ERR_SCALE = -10,        /* scale is not finite                              */
+  SPECMOE_ERR_LAUNCH = -11        /* HIP reported an error for a kernel launch        */
+};
+
+/* Problem description.  Sizes are in elements unless stated otherwise. */
+typedef struct specmoe_verify_desc {
+  int32_t B;          /* sequences in the batch; 0 returns SPECMOE_OK at once, without
+                         looking at any data pointer                              */
+  int32_t Hq;         /* query heads                                                */
+  int32_t Hkv;        /* KV heads; Hq % Hkv == 0, g = Hq / Hkv                      */
+  int32_t D;          /* head dimension: 64 or 128                                  */
+  int32_t C_max;      /* draft-token capacity per sequence (rows of q/out/lse)      */
+  int32_t S_max;      /* token capacity of the KV cache per (sequence, KV head)     */
+  int32_t dtype;      /* specmoe_dtype of q, k_cache, v_cache                       */
+  int32_t split_len;  /* keys per split-KV partition; 0 = chosen by the library.
+                         Must be a multiple of specmoe_verify_attn_key_tile(desc)
+                         and >= C_max.                                             */
+  void* workspace;          /* device; caller-allocated scratch, >= workspace_bytes */
+  size_t workspace_bytes;   /* size of workspace in bytes                           */
+  void* ev_main_begin;      /* optional hipEvent_t recorded on the stream right
+                               before the main kernel (NULL: none)                  */
+  void* ev_main_end;        /* optional hipEvent_t recorded right after it          */
+} specmoe_verify_desc;
+
+/*
+ * specmoe_verify_attn -- chunked verification attention (Section 5.1).
+ *
+ * Arguments (all device pointers, C-contiguous, row-major):
+ *   q          [B, C_max, Hq, D] dtype.  Row (b, i) holds the queries of draft
+ *              token i of sequence b; rows i >= c_b are never read.
+ *   k_cache    [B, Hkv, S_max, D] dtype.  Rows [0, l_b) hold the cached
+ *   v_cache    context, rows [l_b, l_b + c_b) the chunk's own keys/values,
+ *              already appended.  Rows >= l_b + c_b are never read.
+ *   ctx_lens   int32 [B]: l_b, the cached context length of sequence b.
+ *   chunk_lens int32 [B]: c_b, the draft chunk length (gamma + 1) of b.
+ *   scale      softmax scale applied to q.k (e.g. 1/sqrt(D)).
+ *   out        float32 [B, C_max, Hq, D]: attention output.
+ *   lse        float32 [B, C_max, Hq]: natural-log log-sum-exp of the scaled,
+ *              masked scores of each row.
+ *   stream     hipStream_t the work is enqueued on (NULL: the null stream).
+ *   desc       host pointer to the problem description.
+ * Padding rows (c_b <= i < C_max) get out = 0 and lse = -inf.  A sequence with
+ * c_b = 0 has only padding rows.
+ *
+ * Device-side preconditions (not checked on the host, since the lengths live
+ * in device memory and the call never synchronises): 0 <= c_b <= C_max,
+ * l_b >= 0, l_b + c_b <= S_max.  The kernels clamp violating lengths into
+ * these ranges before any memory access, so a violation yields unspecified
+ * values but never an out-of-bounds access.
+ *
+ * Ownership: the caller owns every buffer, including the workspace; the
+ * library allocates nothing, keeps no pointer after returning, and does not
+ * synchronise with the host: the work is asynchronous on `stream`, and the
+ * buffers must stay valid until it completes.  Calls are reentrant; calls
+ * that may run concurrently need distinct workspaces.
+ *
+ * Errors: all host-side checks run before any HIP call; on an error nothing
+ * is enqueued and one of the SPECMOE_ERR_* codes is returned.  A launch
+ * failure reported by HIP returns SPECMOE_ERR_LAUNCH.
+ */
+int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
+                        const int32_t* ctx_lens, const int32_t* chunk_lens,
+                        float scale, float* out, float* lse, void* stream,
+                        const specmoe_verify_desc* desc);
+
+/* Bytes of device workspace specmoe_verify_attn needs for `desc` (its
+ * split_len included).  Returns 0 for an invalid descriptor or when no
+ * workspace is needed. */
+size_t specmoe_verify_attn_workspace_bytes(const specmoe_verify_desc* desc);
+
+/* Split length (keys per split-KV partition) a call with `desc` uses: the
+ * descriptor's split_len if non-zero, otherwise the library's choice.
+ * Returns a negative status for an invalid descriptor. */
+int32_t specmoe_verify_attn_split_len(const specmoe_verify_desc* desc);
+
+/* Keys staged per block iteration for `desc`'s dtype and D; split_len must be
+ * a multiple of it.  Negative status for an invalid dtype or D. */
+int32_t specmoe_verify_attn_key_tile(const specmoe_verify_desc* desc);
+
+/* Static, human-readable text for a status code. */
+const char* specmoe_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPECMOE_VERIFY_H */

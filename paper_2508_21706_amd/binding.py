@@ -1,0 +1,185 @@
+"""Thin Python binding of the chunked verification-attention C-ABI.
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libspecmoe_verify.so``; PyTorch supplies device memory and the
+stream.  There is no fallback path: if the shared library is missing, every
+entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+LIB_NAME = "libspecmoe_verify.so"
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
+
+SPECMOE_F32 = 0
+SPECMOE_BF16 = 1
+
+STATUS = {
+    0: "SPECMOE_OK", -1: "SPECMOE_ERR_NULL_POINTER", -2: "SPECMOE_ERR_SHAPE", -3: "SPECMOE_ERR_GQA",
+    -4: "SPECMOE_ERR_HEAD_DIM", -5: "SPECMOE_ERR_DTYPE", -6: "SPECMOE_ERR_ROWS", -7: "SPECMOE_ERR_SPLIT",
+    -8: "SPECMOE_ERR_WORKSPACE", -9: "SPECMOE_ERR_ALIGN", -10: "SPECMOE_ERR_SCALE", -11: "SPECMOE_ERR_LAUNCH",
+}
+
+
+class Desc(ctypes.Structure):
+    """Mirror of ``specmoe_verify_desc``."""
+    _fields_ = [
+        ("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32), ("D", ctypes.c_int32),
+        ("C_max", ctypes.c_int32), ("S_max", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("split_len", ctypes.c_int32),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+        ("ev_main_begin", ctypes.c_void_p), ("ev_main_end", ctypes.c_void_p),
+    ]
+
+
+class SpecMoEError(RuntimeError):
+    def __init__(self, status: int, text: str):
+        super().__init__(f"{STATUS.get(status, status)}: {text}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load the HIP library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(
+            f"{p} is missing: build the HIP library first (python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(p)
+    lib.specmoe_verify_attn.restype = ctypes.c_int
+    lib.specmoe_verify_attn.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_workspace_bytes.restype = ctypes.c_size_t
+    lib.specmoe_verify_attn_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_split_len.restype = ctypes.c_int32
+    lib.specmoe_verify_attn_split_len.argtypes = [ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_key_tile.restype = ctypes.c_int32
+    lib.specmoe_verify_attn_key_tile.argtypes = [ctypes.POINTER(Desc)]
+    lib.specmoe_status_str.restype = ctypes.c_char_p
+    lib.specmoe_status_str.argtypes = [ctypes.c_int]
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def status_str(status: int) -> str:
+    return load_library().specmoe_status_str(status).decode()
+
+
+def make_desc(B, Hq, Hkv, D, C_max, S_max, dtype: int, split_len: int = 0,
+              workspace: Optional[torch.Tensor] = None, events=None) -> Desc:
+    d = Desc(B, Hq, Hkv, D, C_max, S_max, dtype, split_len, None, 0, None, None)
+    if workspace is not None:
+        d.workspace = workspace.data_ptr()
+        d.workspace_bytes = workspace.numel() * workspace.element_size()
+    if events is not None:
+        d.ev_main_begin, d.ev_main_end = events
+    return d
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return SPECMOE_BF16
+    if t.dtype == torch.float32:
+        return SPECMOE_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; expected torch.bfloat16 or torch.float32")
+
+
+def desc_for(q: torch.Tensor, k_cache: torch.Tensor, split_len: int = 0) -> Desc:
+    B, C_max, Hq, D = q.shape
+    _, Hkv, S_max, _ = k_cache.shape
+    return make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), split_len)
+
+
+def workspace_bytes(desc: Desc) -> int:
+    return int(load_library().specmoe_verify_attn_workspace_bytes(ctypes.byref(desc)))
+
+
+def split_len(desc: Desc) -> int:
+    return int(load_library().specmoe_verify_attn_split_len(ctypes.byref(desc)))
+
+
+def key_tile(desc: Desc) -> int:
+    return int(load_library().specmoe_verify_attn_key_tile(ctypes.byref(desc)))
+
+
+def alloc_workspace(desc: Desc, device) -> Optional[torch.Tensor]:
+    n = workspace_bytes(desc)
+    if n == 0:
+        return None
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def _check(t: torch.Tensor, name: str, shape, dtype):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                ctx_lens: torch.Tensor, chunk_lens: torch.Tensor, scale: float,
+                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, split_len: int = 0,
+                stream: Optional[torch.cuda.Stream] = None, events=None,
+                check_lengths: bool = False):
+    """Chunked verification attention; see ``include/specmoe_verify.h``.
+
+    q [B, C_max, Hq, D], k_cache / v_cache [B, Hkv, S_max, D] (bf16 or f32),
+    ctx_lens / chunk_lens int32 [B], all on the GPU.  Returns (out, lse) as
+    float32 [B, C_max, Hq, D] and [B, C_max, Hq].  ``check_lengths`` copies the
+    lengths to the host (a synchronisation) and checks the kernel's
+    preconditions; off by default.
+    """
+    lib = load_library()
+    B, C_max, Hq, D = q.shape
+    if k_cache.dim() != 4:
+        raise ValueError("k_cache must be [B, Hkv, S_max, D]")
+    _, Hkv, S_max, _ = k_cache.shape
+    dt = q.dtype
+    _check(q, "q", (B, C_max, Hq, D), dt)
+    _check(k_cache, "k_cache", (B, Hkv, S_max, D), dt)
+    _check(v_cache, "v_cache", (B, Hkv, S_max, D), dt)
+    _check(ctx_lens, "ctx_lens", (B,), torch.int32)
+    _check(chunk_lens, "chunk_lens", (B,), torch.int32)
+    if check_lengths:
+        c = chunk_lens.cpu()
+        l = ctx_lens.cpu()
+        if (c < 0).any() or (c > C_max).any() or (l < 0).any() or (l + c > S_max).any():
+            raise ValueError("lengths break 0 <= c_b <= C_max, l_b >= 0, l_b + c_b <= S_max")
+    if out is None:
+        out = torch.empty((B, C_max, Hq, D), dtype=torch.float32, device=q.device)
+    if lse is None:
+        lse = torch.empty((B, C_max, Hq), dtype=torch.float32, device=q.device)
+    _check(out, "out", (B, C_max, Hq, D), torch.float32)
+    _check(lse, "lse", (B, C_max, Hq), torch.float32)
+    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), split_len)
+    if workspace is None:
+        workspace = alloc_workspace(desc, q.device)
+    if workspace is not None:
+        desc.workspace = workspace.data_ptr()
+        desc.workspace_bytes = workspace.numel() * workspace.element_size()
+    if events is not None:
+        desc.ev_main_begin, desc.ev_main_end = events
+    s = stream if stream is not None else torch.cuda.current_stream(q.device)
+    st = lib.specmoe_verify_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                 ctx_lens.data_ptr(), chunk_lens.data_ptr(), float(scale),
+                                 out.data_ptr(), lse.data_ptr(), s.cuda_stream, ctypes.byref(desc))
+    if st != 0:
+        raise SpecMoEError(st, status_str(st))
+    return out, lse

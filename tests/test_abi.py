@@ -1,0 +1,121 @@
+"""Host-only checks of the C-ABI library: it loads, exports every function the
+header declares, and rejects invalid arguments before making any HIP call (so
+these run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2508_21706_amd import binding as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "specmoe_verify.h")
+
+FAKE = 0x10000          # 16-byte aligned, never dereferenced by these tests
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return bd.load_library()
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(specmoe_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_function(lib):
+    names = header_functions()
+    assert {"specmoe_verify_attn", "specmoe_verify_attn_workspace_bytes",
+            "specmoe_status_str"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} is declared in the header but not exported"
+
+
+def test_status_codes_match_header(lib):
+    text = open(HEADER).read()
+    codes = dict((n, int(v)) for n, v in re.findall(r"(SPECMOE_(?:OK|ERR_\w+))\s*=\s*(-?\d+)", text))
+    assert codes == {v: k for k, v in bd.STATUS.items()}
+    for code in codes.values():
+        assert lib.specmoe_status_str(code).decode() not in ("", "unknown status")
+    assert lib.specmoe_status_str(12345).decode() == "unknown status"
+
+
+def _desc(**kw):
+    base = dict(B=2, Hq=32, Hkv=8, D=128, C_max=5, S_max=2304, dtype=bd.SPECMOE_BF16, split_len=0)
+    base.update(kw)
+    return bd.make_desc(**base)
+
+
+def _call(lib, desc, q=FAKE, k=FAKE, v=FAKE, ctx=FAKE, chunk=FAKE, scale=0.088, out=FAKE, lse=FAKE):
+    return lib.specmoe_verify_attn(q, k, v, ctx, chunk, scale, out, lse, None,
+                                   ctypes.byref(desc) if desc is not None else None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=7), -5),
+    (dict(D=96), -4),
+    (dict(D=256), -4),
+    (dict(B=-1), -2),
+    (dict(Hq=0), -2),
+    (dict(Hkv=0), -2),
+    (dict(C_max=0), -2),
+    (dict(S_max=4, C_max=5), -2),
+    (dict(Hq=30, Hkv=8), -3),
+    (dict(C_max=17, Hq=32, Hkv=4), -6),          # 17 * 8 = 136 rows > 128
+    (dict(split_len=100), -7),                   # not a multiple of the key tile
+    (dict(split_len=-128), -7),
+    (dict(S_max=1 << 24), -2),                   # slab offsets would pass 2^31 bytes
+])
+def test_invalid_descriptor(lib, kw, code):
+    assert _call(lib, _desc(**kw)) == code
+    assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(_desc(**kw))) == 0
+
+
+def test_null_and_alignment_and_scale(lib):
+    d = _desc()
+    assert _call(lib, None) == -1
+    for arg in ("q", "k", "v", "ctx", "chunk", "out", "lse"):
+        assert _call(lib, d, **{arg: None}) == -1, arg
+    for arg in ("q", "k", "v", "out"):
+        assert _call(lib, d, **{arg: FAKE + 4}) == -9, arg
+    assert _call(lib, d, scale=float("nan")) == -10
+    assert _call(lib, d, scale=float("inf")) == -10
+
+
+def test_workspace_contract(lib):
+    d = _desc(B=64, split_len=512)             # 2304 / 512 -> 5 splits per unit
+    need = lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d))
+    rows = 5 * 4                                # C_max * g
+    slots = 64 * 8 * 5 * rows
+    assert need >= slots * (128 + 1) * 4
+    assert need < slots * (128 + 1) * 4 + 256
+    assert _call(lib, d) == -1                  # workspace needed but NULL
+    d.workspace, d.workspace_bytes = FAKE, need - 1
+    assert _call(lib, d) == -8
+    d.workspace, d.workspace_bytes = FAKE + 8, need
+    assert _call(lib, d) == -9
+    # one split per unit needs no workspace
+    d1 = _desc(B=64, split_len=2304)
+    assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d1)) == 0
+
+
+def test_split_len_choice(lib):
+    d = _desc(B=64)
+    tile = lib.specmoe_verify_attn_key_tile(ctypes.byref(d))
+    assert tile == 128                          # 32 KB of bf16 D=128 rows
+    L = lib.specmoe_verify_attn_split_len(ctypes.byref(d))
+    assert L % tile == 0 and L >= 5
+    assert lib.specmoe_verify_attn_split_len(ctypes.byref(_desc(split_len=256))) == 256
+    assert lib.specmoe_verify_attn_split_len(ctypes.byref(_desc(D=80))) == -4
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=64))) == 128
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=128))) == 64
+
+
+def test_empty_batch_is_a_no_op(lib):
+    # B = 0 returns before any HIP call and before looking at data pointers
+    assert _call(lib, _desc(B=0)) == 0
+    assert _call(lib, _desc(B=0), q=None, k=None, v=None, ctx=None, chunk=None, out=None, lse=None) == 0
+    assert _call(lib, _desc(B=0, dtype=9)) == -5    # the descriptor is still validated

@@ -1,0 +1,241 @@
+"""GPU parity: the HIP path through the C-ABI against the fp64 CPU oracle.
+
+Tolerances (written here, applied to every valid row):
+  * f32 inputs:  max |out - ref| <= 1e-4 and max |lse - ref| <= 1e-4
+  * bf16 inputs: max |out - ref| <= 1e-2 and max |lse - ref| <= 1e-3
+Padding rows (i >= c_b) must be exactly out = 0, lse = -inf.  Unused cache
+rows and query rows are NaN-poisoned, so any read of them shows up as NaN.
+"""
+import dataclasses
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2508_21706_amd as pkg
+from paper_2508_21706_amd import workloads as wl
+from oracle import verify_attn_ref
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": (1e-4, 1e-4), "bf16": (1e-2, 1e-3)}
+
+
+def dev():
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU tests need a GPU")
+    return torch.device("cuda:0")
+
+
+def to_dev(a, dtype):
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev())
+    return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev())
+
+
+def note(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def run_gpu(inp, dtype, split_len=0):
+    out, lse = pkg.verify_attn(to_dev(inp["q"], dtype), to_dev(inp["k_cache"], dtype),
+                               to_dev(inp["v_cache"], dtype),
+                               torch.from_numpy(np.asarray(inp["ctx_lens"], np.int32)).to(dev()),
+                               torch.from_numpy(np.asarray(inp["chunk_lens"], np.int32)).to(dev()),
+                               inp["scale"], split_len=split_len, check_lengths=True)
+    torch.cuda.synchronize()
+    return out.cpu().double().numpy(), lse.cpu().double().numpy()
+
+
+def compare(o, s, ref_o, ref_l, dtype, label, units=None):
+    tol_o, tol_l = TOL[dtype]
+    computed = ~np.isnan(ref_l)                 # rows of units the oracle computed
+    valid = computed & np.isfinite(ref_l)
+    pad = computed & ~np.isfinite(ref_l)
+    assert valid.any()
+    err_o = np.abs(o[valid] - ref_o[valid])
+    err_l = np.abs(s[valid] - ref_l[valid])
+    rms = np.sqrt(np.mean(ref_o[valid] ** 2))
+    note(f"[{label}] rows={int(valid.sum())} max|dout|={err_o.max():.3e} "
+         f"(rel RMS {err_o.max() / rms:.3e}) max|dlse|={err_l.max():.3e} pad_rows={int(pad.sum())}")
+    assert np.all(np.isfinite(o[valid])), "non-finite output in a valid row"
+    assert err_o.max() <= tol_o, f"{label}: out error {err_o.max():.3e} > {tol_o}"
+    assert err_l.max() <= tol_l, f"{label}: lse error {err_l.max():.3e} > {tol_l}"
+    assert np.all(o[pad] == 0.0), f"{label}: padding rows of out are not zero"
+    assert np.all(s[pad] == -np.inf), f"{label}: padding rows of lse are not -inf"
+
+
+def check_case(inp, dtype, label, split_len=0):
+    note(f"case {label} split_len={split_len}")
+    o, s = run_gpu(inp, dtype, split_len)
+    ref_o, ref_l = verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], inp["ctx_lens"],
+                                   inp["chunk_lens"], inp["scale"], dtype)
+    compare(o, s, ref_o, ref_l, dtype, label)
+    return o, s
+
+
+# ------------------------------------------------------------- workloads
+
+def test_tiny_fp32_full():
+    w = wl.get("tiny_fp32")
+    inp = wl.make_inputs(w)
+    for L in (0, 128):
+        check_case(inp, w.dtype, w.name, split_len=L)
+
+
+@pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128"])
+def test_workload_reduced_batch(name):
+    """Every row of a few sequences drawn from each workload's distribution."""
+    w = wl.get(name)
+    nb = 3 if name == "long_ctx_b32" else 6
+    w = dataclasses.replace(w, B=nb)
+    inp = wl.make_inputs(w)
+    tile = 128
+    for L in (0, tile, 4 * tile, w.S_max):
+        check_case(inp, w.dtype, f"{name}[B={nb}]", split_len=L)
+
+
+def _full_size_inputs(w, sample):
+    """Full-size workload on the GPU: every sequence holds N(0,1) bf16 from
+    torch's generator except the sampled ones, which hold the recipe's values
+    (NaN-poisoned outside their valid rows) and are checked by the oracle."""
+    ctx, chunk = wl.draw_lengths(w)
+    d = dev()
+    g = torch.Generator(device=d)
+    g.manual_seed(1000 + w.index)
+    shape = (w.B, w.Hkv, w.S_max, w.D)
+    k = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(torch.bfloat16)
+    host = wl.make_inputs(w, batches=sample)
+    for b in sample:
+        k[b] = to_dev(host["k_cache"][b], "bf16")
+        v[b] = to_dev(host["v_cache"][b], "bf16")
+    return host, to_dev(host["q"], "bf16"), k, v, ctx, chunk
+
+
+@pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128"])
+def test_workload_full_size_sampled(name):
+    """Full-size workload in the benchmark's launch configuration (automatic
+    split length); the oracle checks sampled sequences, every output row is
+    checked for finiteness and padding."""
+    w = wl.get(name)
+    ctx, chunk = wl.draw_lengths(w)
+    rng = np.random.default_rng(77)
+    sample = sorted({0, w.B - 1, int(np.argmin(ctx)), int(np.argmax(ctx)),
+                     *rng.choice(w.B, 2, replace=False).tolist()})
+    note(f"case {name} full size, sampled sequences {sample}")
+    host, q, k, v, ctx, chunk = _full_size_inputs(w, sample)
+    d = dev()
+    out, lse = pkg.verify_attn(q, k, v, torch.from_numpy(ctx).to(d), torch.from_numpy(chunk).to(d), w.scale)
+    torch.cuda.synchronize()
+    units = [(b, h) for b in sample for h in range(w.Hkv)]
+    ref_o, ref_l = verify_attn_ref(host["q"], host["k_cache"], host["v_cache"], ctx, chunk, w.scale,
+                                   w.dtype, units=units)
+    o = out.cpu().double().numpy()
+    s = lse.cpu().double().numpy()
+    compare(o, s, ref_o, ref_l, w.dtype, f"{name} full-size sampled")
+    # every row of the whole batch: finite where valid, exact padding elsewhere
+    rows = np.arange(w.C_max)[None, :] < chunk[:, None]
+    assert np.all(np.isfinite(o[rows])) and np.all(np.isfinite(s[rows]))
+    assert np.all(o[~rows] == 0.0) and np.all(s[~rows] == -np.inf)
+    del k, v, q, out, lse
+    torch.cuda.empty_cache()
+
+
+# ------------------------------------------------------------- edge cases
+
+def _custom(B, Hq, Hkv, D, dtype, ctx, chunk, C_max, seed=5):
+    """Seeded inputs with the given lengths; capacity S_max = max(ctx) + C_max
+    rounded up to 256, NaN beyond each sequence's valid rows."""
+    ctx = np.asarray(ctx, np.int32)
+    chunk = np.asarray(chunk, np.int32)
+    w = wl.Workload("edge", seed, B=B, Hq=Hq, Hkv=Hkv, D=D, dtype=dtype, ctx=("fixed", list(ctx)),
+                    chunk=("uniform", 0, C_max), description="edge case")
+    return wl.make_inputs(w, ctx_lens=ctx, chunk_lens=chunk)
+
+
+EDGE = {
+    # name: (B, Hq, Hkv, D, dtype, ctx, chunk, C_max)
+    "zero_chunk_and_zero_ctx": (4, 8, 2, 128, "bf16", [0, 300, 0, 17], [3, 0, 1, 4], 4),
+    "single_key": (2, 4, 4, 128, "bf16", [0, 0], [1, 1], 1),
+    "tile_boundaries": (6, 8, 2, 128, "bf16", [123, 127, 128, 129, 255, 507], [5, 1, 2, 5, 1, 5], 5),
+    "three_row_tiles": (4, 28, 4, 128, "bf16", [700, 33, 1500, 2], [10, 12, 13, 16], 16),
+    "max_rows_128": (2, 32, 4, 128, "bf16", [900, 64], [16, 16], 16),
+    "mha_g1": (3, 8, 8, 128, "bf16", [400, 10, 1000], [4, 2, 3], 4),
+    "bf16_d64": (3, 16, 4, 64, "bf16", [500, 260, 1], [5, 3, 5], 5),
+    "f32_d128": (2, 8, 2, 128, "f32", [300, 77], [4, 2], 4),
+    "f32_d64_many": (3, 12, 3, 64, "f32", [1000, 5, 640], [3, 8, 1], 8),
+}
+
+
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_edge_case(name):
+    B, Hq, Hkv, D, dtype, ctx, chunk, C_max = EDGE[name]
+    inp = _custom(B, Hq, Hkv, D, dtype, ctx, chunk, C_max)
+    w = pkg.desc_for(torch.empty((B, C_max, Hq, D), dtype=torch.float32 if dtype == "f32" else torch.bfloat16),
+                     torch.empty((B, Hkv, inp["k_cache"].shape[2], D)))
+    tile = pkg.key_tile(w)
+    for L in (0, tile, 2 * tile):
+        check_case(inp, dtype, name, split_len=L)
+
+
+def test_mask_leak_is_visible():
+    """Draft keys get scores far above the context's: a row that saw a key
+    beyond its own position would be dominated by it."""
+    B, Hq, Hkv, D, C = 2, 8, 2, 128, 5
+    inp = _custom(B, Hq, Hkv, D, "bf16", [200, 333], [5, 4], C)
+    k = inp["k_cache"].view(np.uint16)
+    qv = (inp["q"].astype(np.uint32) << 16).view(np.float32)
+    for b in range(B):
+        l, n = int(inp["ctx_lens"][b]), int(inp["chunk_lens"][b])
+        for h in range(Hkv):
+            # draft key j aligned with every query of the sequence, scaled up
+            direction = qv[b, :n, h * 4:(h + 1) * 4].reshape(-1, D).mean(axis=0)
+            for j in range(n):
+                k[b, h, l + j] = wl.f32_to_bf16_bits((direction * (8.0 + 4.0 * j)).astype(np.float32))
+    # one-hot V rows for the draft keys expose the weights directly
+    v = inp["v_cache"]
+    for b in range(B):
+        l, n = int(inp["ctx_lens"][b]), int(inp["chunk_lens"][b])
+        for j in range(n):
+            row = np.zeros(D, np.float32)
+            row[j] = 1.0
+            v[b, :, l + j] = wl.f32_to_bf16_bits(row)
+    check_case(inp, "bf16", "mask_leak_structured")
+
+
+def test_repeat_is_bitwise_deterministic():
+    w = dataclasses.replace(wl.get("ragged_chunk_b128"), B=4)
+    inp = wl.make_inputs(w)
+    o1, s1 = run_gpu(inp, w.dtype, split_len=256)
+    for _ in range(3):
+        o2, s2 = run_gpu(inp, w.dtype, split_len=256)
+        assert np.array_equal(o1, o2) and np.array_equal(s1, s2)
+
+
+def test_lengths_outside_preconditions_stay_in_bounds():
+    """Lengths that break the documented preconditions are clamped by the
+    kernels: the call completes and padding/valid rows stay well formed."""
+    B, Hq, Hkv, D, C = 3, 8, 2, 128, 4
+    d = dev()
+    ctx = torch.tensor([-5, 10 ** 6, 10], dtype=torch.int32, device=d)
+    chunk = torch.tensor([2, 2, 99], dtype=torch.int32, device=d)
+    # the whole cache holds finite values here, so clamped reads stay finite
+    k = torch.randn((B, Hkv, 64, D), device=d).to(torch.bfloat16)
+    v = torch.randn((B, Hkv, 64, D), device=d).to(torch.bfloat16)
+    q = torch.randn((B, C, Hq, D), device=d).to(torch.bfloat16)
+    out, lse = pkg.verify_attn(q, k, v, ctx, chunk, 0.088)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all()
+    assert torch.isfinite(lse[:, :2]).all()
+
+
+def test_empty_batch():
+    d = dev()
+    q = torch.empty((0, 4, 8, 128), dtype=torch.bfloat16, device=d)
+    k = torch.empty((0, 2, 64, 128), dtype=torch.bfloat16, device=d)
+    e = torch.empty((0,), dtype=torch.int32, device=d)
+    out, lse = pkg.verify_attn(q, k, k, e, e, 0.1)
+    assert out.shape == (0, 4, 8, 128) and lse.shape == (0, 4, 8)
