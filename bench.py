@@ -1,8 +1,8 @@
 """Benchmark: chunked verification attention on one MI355X.
 
-One step = one call of the whole hot path (main split-KV kernel + combine
-kernel) over one batch of the synthetic workload, with every input already
-resident in HBM.  Prints ONE JSON line on stdout; progress goes to stderr.
+One step = one call of the whole hot path (the single persistent kernel that
+streams the KV cache and merges split units) over one batch of the synthetic
+workload, with every input already resident in HBM.  Prints ONE JSON line on stdout; progress goes to stderr.
 
     python bench.py [--steps K] [--warmup W] [--workload mixtral_b64]
 
@@ -29,7 +29,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "effective KV HBM GB/s and verified draft tokens/sec, Mixtral shape B=64"
 HBM_PEAK_GBS = 8000.0
-MAIN_KERNEL = "verify_main_kernel"
+MAIN_KERNEL = "verify_attn_kernel"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2508_21706_amd", "csrc", "verify_attn.hip")
 
 
@@ -98,7 +98,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mixtral_b64")
-    ap.add_argument("--split-len", type=int, default=0)
+    ap.add_argument("--grid-blocks", type=int, default=0, help="persistent workgroups (0: library default)")
     ap.add_argument("--rotate", type=int, default=0, help="input sets (0: enough for >= 1 GB)")
     ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work; 0 skips")
     args = ap.parse_args()
@@ -138,19 +138,18 @@ def main():
     sets = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_sets - 1)]
     ctx_d = torch.from_numpy(ctx).to(dev)
     chunk_d = torch.from_numpy(chunk).to(dev)
-    desc = pkg.desc_for(q, k0, args.split_len)
-    L = pkg.split_len(desc)
+    desc = pkg.desc_for(q, k0, args.grid_blocks)
     ws = pkg.alloc_workspace(desc, dev)
     out = torch.empty((w.B, w.C_max, w.Hq, w.D), dtype=torch.float32, device=dev)
     lse = torch.empty((w.B, w.C_max, w.Hq), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
-    log(f"{n_sets} input sets x {set_bytes / 1e6:.0f} MB, split_len={L}, "
+    log(f"{n_sets} input sets x {set_bytes / 1e6:.0f} MB, grid_blocks={args.grid_blocks or 'default'}, "
         f"KV bytes/step={kv_bytes / 1e6:.1f} MB, draft tokens/step={tokens}")
 
     def step(i, events=None):
         k, v = sets[i % n_sets]
         pkg.verify_attn(q, k, v, ctx_d, chunk_d, w.scale, out=out, lse=lse, workspace=ws,
-                        split_len=args.split_len, stream=stream, events=events)
+                        grid_blocks=args.grid_blocks, stream=stream, events=events)
 
     for i in range(args.warmup):
         step(i)
@@ -209,7 +208,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
                    "head_dim": w.D, "ctx_lens_sum": int(ctx.sum()), "chunk_lens_sum": tokens,
-                   "C_max": w.C_max, "S_max": w.S_max, "split_len": L, "input_sets": n_sets,
+                   "C_max": w.C_max, "S_max": w.S_max, "grid_blocks": args.grid_blocks or 512,
+                   "input_sets": n_sets,
                    "parallelism": "single GPU"},
         "verified_tokens_per_s": round(tokens / t, 1),
         "kv_bytes_per_step": kv_bytes,

@@ -45,8 +45,8 @@ enum {
   SPECMOE_ERR_HEAD_DIM = -4,      /* D is not 64 or 128                               */
   SPECMOE_ERR_DTYPE = -5,         /* dtype is not a specmoe_dtype value               */
   SPECMOE_ERR_ROWS = -6,          /* C_max * (Hq / Hkv) > 128 query rows per KV head  */
-  SPECMOE_ERR_SPLIT = -7,         /* split_len is not 0 and not a positive multiple of
-                                     the key tile, or it is smaller than C_max        */
+  SPECMOE_ERR_GRID = -7,          /* grid_blocks is negative, larger than 2^20, or so
+                                     large that partial results would pass 2 GB       */
   SPECMOE_ERR_WORKSPACE = -8,     /* workspace smaller than the size query returns    */
   SPECMOE_ERR_ALIGN = -9,         /* q, k_cache, v_cache, out or workspace is not
                                      16-byte aligned                                  */
@@ -64,10 +64,10 @@ typedef struct specmoe_verify_desc {
   int32_t C_max;      /* draft-token capacity per sequence (rows of q/out/lse)      */
   int32_t S_max;      /* token capacity of the KV cache per (sequence, KV head)     */
   int32_t dtype;      /* specmoe_dtype of q, k_cache, v_cache                       */
-  int32_t split_len;  /* keys per split-KV partition; 0 = chosen by the library.
-                         Must be a multiple of specmoe_verify_attn_key_tile(desc)
-                         and >= C_max.                                             */
-  void* workspace;          /* device; caller-allocated scratch, >= workspace_bytes */
+  int32_t grid_blocks;  /* persistent workgroups that share the key tiles; 0 = the
+                           library default (512: two per CU of an MI355X)          */
+  void* workspace;          /* device; caller-allocated scratch, >= workspace_bytes,
+                               whose counter region is zero (see below)             */
   size_t workspace_bytes;   /* size of workspace in bytes                           */
   void* ev_main_begin;      /* optional hipEvent_t recorded on the stream right
                                before the main kernel (NULL: none)                  */
@@ -76,6 +76,12 @@ typedef struct specmoe_verify_desc {
 
 /*
  * specmoe_verify_attn -- chunked verification attention (Section 5.1).
+ *
+ * Work split: the keys of every (sequence, KV head) are cut into tiles, and
+ * the tiles of all of them are divided evenly among `grid_blocks` persistent
+ * workgroups.  A (sequence, KV head) whose tiles span several workgroups is
+ * computed in pieces that are merged with log-sum-exp weights -- the
+ * sequence-dimension KV partition of Section 5.2 -- through the workspace.
  *
  * Arguments (all device pointers, C-contiguous, row-major):
  *   q          [B, C_max, Hq, D] dtype.  Row (b, i) holds the queries of draft
@@ -104,7 +110,9 @@ typedef struct specmoe_verify_desc {
  * library allocates nothing, keeps no pointer after returning, and does not
  * synchronise with the host: the work is asynchronous on `stream`, and the
  * buffers must stay valid until it completes.  Calls are reentrant; calls
- * that may run concurrently need distinct workspaces.
+ * that may run concurrently need distinct workspaces.  The workspace's
+ * counter region must be zero when the call starts (see
+ * specmoe_verify_attn_workspace_bytes); the call leaves it zero.
  *
  * Errors: all host-side checks run before any HIP call; on an error nothing
  * is enqueued and one of the SPECMOE_ERR_* codes is returned.  A launch
@@ -116,17 +124,23 @@ int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
                         const specmoe_verify_desc* desc);
 
 /* Bytes of device workspace specmoe_verify_attn needs for `desc` (its
- * split_len included).  Returns 0 for an invalid descriptor or when no
- * workspace is needed. */
+ * grid_blocks included); 0 for an invalid descriptor.  The workspace holds
+ * per-(sequence, KV head) arrival counters followed by the partial results of
+ * pieces.  The counters must be zero when a call starts; every call that
+ * completes leaves them zero again, so a workspace zeroed once (for instance
+ * by specmoe_verify_attn_workspace_init) can be reused for any number of
+ * calls with the same or a smaller descriptor. */
 size_t specmoe_verify_attn_workspace_bytes(const specmoe_verify_desc* desc);
 
-/* Split length (keys per split-KV partition) a call with `desc` uses: the
- * descriptor's split_len if non-zero, otherwise the library's choice.
- * Returns a negative status for an invalid descriptor. */
-int32_t specmoe_verify_attn_split_len(const specmoe_verify_desc* desc);
+/* Zero the counter region of `workspace` (device, workspace_bytes long) with
+ * a small kernel on `stream` (a hipStream_t; NULL: the null stream).  Status:
+ * SPECMOE_OK, a descriptor error, SPECMOE_ERR_NULL_POINTER, SPECMOE_ERR_ALIGN,
+ * SPECMOE_ERR_WORKSPACE if the buffer is too small, or SPECMOE_ERR_LAUNCH. */
+int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, void* stream,
+                                       const specmoe_verify_desc* desc);
 
-/* Keys staged per block iteration for `desc`'s dtype and D; split_len must be
- * a multiple of it.  Negative status for an invalid dtype or D. */
+/* Keys per tile for `desc`'s dtype and D (32 KB of K rows).  Negative status
+ * for an invalid dtype or D. */
 int32_t specmoe_verify_attn_key_tile(const specmoe_verify_desc* desc);
 
 /* Static, human-readable text for a status code. */

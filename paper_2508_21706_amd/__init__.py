@@ -4,4 +4,4 @@
 C-ABI; ``workloads`` draws the seeded synthetic inputs.
 """
 from .binding import (Desc, SpecMoEError, alloc_workspace, desc_for, key_tile,  # noqa: F401
-                      load_library, make_desc, split_len, status_str, verify_attn, workspace_bytes)
+                      load_library, make_desc, status_str, verify_attn, workspace_bytes)

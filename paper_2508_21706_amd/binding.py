@@ -21,7 +21,7 @@ SPECMOE_BF16 = 1
 
 STATUS = {
     0: "SPECMOE_OK", -1: "SPECMOE_ERR_NULL_POINTER", -2: "SPECMOE_ERR_SHAPE", -3: "SPECMOE_ERR_GQA",
-    -4: "SPECMOE_ERR_HEAD_DIM", -5: "SPECMOE_ERR_DTYPE", -6: "SPECMOE_ERR_ROWS", -7: "SPECMOE_ERR_SPLIT",
+    -4: "SPECMOE_ERR_HEAD_DIM", -5: "SPECMOE_ERR_DTYPE", -6: "SPECMOE_ERR_ROWS", -7: "SPECMOE_ERR_GRID",
     -8: "SPECMOE_ERR_WORKSPACE", -9: "SPECMOE_ERR_ALIGN", -10: "SPECMOE_ERR_SCALE", -11: "SPECMOE_ERR_LAUNCH",
 }
 
@@ -31,7 +31,7 @@ class Desc(ctypes.Structure):
     _fields_ = [
         ("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32), ("D", ctypes.c_int32),
         ("C_max", ctypes.c_int32), ("S_max", ctypes.c_int32), ("dtype", ctypes.c_int32),
-        ("split_len", ctypes.c_int32),
+        ("grid_blocks", ctypes.c_int32),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
         ("ev_main_begin", ctypes.c_void_p), ("ev_main_end", ctypes.c_void_p),
     ]
@@ -62,8 +62,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Desc)]
     lib.specmoe_verify_attn_workspace_bytes.restype = ctypes.c_size_t
     lib.specmoe_verify_attn_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
-    lib.specmoe_verify_attn_split_len.restype = ctypes.c_int32
-    lib.specmoe_verify_attn_split_len.argtypes = [ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_workspace_init.restype = ctypes.c_int
+    lib.specmoe_verify_attn_workspace_init.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                                       ctypes.POINTER(Desc)]
     lib.specmoe_verify_attn_key_tile.restype = ctypes.c_int32
     lib.specmoe_verify_attn_key_tile.argtypes = [ctypes.POINTER(Desc)]
     lib.specmoe_status_str.restype = ctypes.c_char_p
@@ -77,9 +78,9 @@ def status_str(status: int) -> str:
     return load_library().specmoe_status_str(status).decode()
 
 
-def make_desc(B, Hq, Hkv, D, C_max, S_max, dtype: int, split_len: int = 0,
+def make_desc(B, Hq, Hkv, D, C_max, S_max, dtype: int, grid_blocks: int = 0,
               workspace: Optional[torch.Tensor] = None, events=None) -> Desc:
-    d = Desc(B, Hq, Hkv, D, C_max, S_max, dtype, split_len, None, 0, None, None)
+    d = Desc(B, Hq, Hkv, D, C_max, S_max, dtype, grid_blocks, None, 0, None, None)
     if workspace is not None:
         d.workspace = workspace.data_ptr()
         d.workspace_bytes = workspace.numel() * workspace.element_size()
@@ -96,29 +97,31 @@ def _dtype_code(t: torch.Tensor) -> int:
     raise TypeError(f"unsupported dtype {t.dtype}; expected torch.bfloat16 or torch.float32")
 
 
-def desc_for(q: torch.Tensor, k_cache: torch.Tensor, split_len: int = 0) -> Desc:
+def desc_for(q: torch.Tensor, k_cache: torch.Tensor, grid_blocks: int = 0) -> Desc:
     B, C_max, Hq, D = q.shape
     _, Hkv, S_max, _ = k_cache.shape
-    return make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), split_len)
+    return make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks)
 
 
 def workspace_bytes(desc: Desc) -> int:
     return int(load_library().specmoe_verify_attn_workspace_bytes(ctypes.byref(desc)))
 
 
-def split_len(desc: Desc) -> int:
-    return int(load_library().specmoe_verify_attn_split_len(ctypes.byref(desc)))
-
-
 def key_tile(desc: Desc) -> int:
     return int(load_library().specmoe_verify_attn_key_tile(ctypes.byref(desc)))
 
 
-def alloc_workspace(desc: Desc, device) -> Optional[torch.Tensor]:
+def alloc_workspace(desc: Desc, device, stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Allocate a workspace for ``desc`` and zero its counters on the stream."""
     n = workspace_bytes(desc)
     if n == 0:
-        return None
-    return torch.empty(n, dtype=torch.uint8, device=device)
+        raise SpecMoEError(-2, "invalid descriptor")
+    ws = torch.empty(n, dtype=torch.uint8, device=device)
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    st = load_library().specmoe_verify_attn_workspace_init(ws.data_ptr(), n, s.cuda_stream, ctypes.byref(desc))
+    if st != 0:
+        raise SpecMoEError(st, status_str(st))
+    return ws
 
 
 def _check(t: torch.Tensor, name: str, shape, dtype):
@@ -135,14 +138,16 @@ def _check(t: torch.Tensor, name: str, shape, dtype):
 def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                 ctx_lens: torch.Tensor, chunk_lens: torch.Tensor, scale: float,
                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
-                workspace: Optional[torch.Tensor] = None, split_len: int = 0,
+                workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
                 stream: Optional[torch.cuda.Stream] = None, events=None,
                 check_lengths: bool = False):
     """Chunked verification attention; see ``include/specmoe_verify.h``.
 
     q [B, C_max, Hq, D], k_cache / v_cache [B, Hkv, S_max, D] (bf16 or f32),
     ctx_lens / chunk_lens int32 [B], all on the GPU.  Returns (out, lse) as
-    float32 [B, C_max, Hq, D] and [B, C_max, Hq].  ``check_lengths`` copies the
+    float32 [B, C_max, Hq, D] and [B, C_max, Hq].  ``workspace`` (from
+    ``alloc_workspace``) is reused across calls; without one, a fresh
+    workspace is allocated and zeroed.  ``check_lengths`` copies the
     lengths to the host (a synchronisation) and checks the kernel's
     preconditions; off by default.
     """
@@ -168,15 +173,16 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
         lse = torch.empty((B, C_max, Hq), dtype=torch.float32, device=q.device)
     _check(out, "out", (B, C_max, Hq, D), torch.float32)
     _check(lse, "lse", (B, C_max, Hq), torch.float32)
-    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), split_len)
+    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks)
+    s = stream if stream is not None else torch.cuda.current_stream(q.device)
+    if B == 0:
+        return out, lse
     if workspace is None:
-        workspace = alloc_workspace(desc, q.device)
-    if workspace is not None:
-        desc.workspace = workspace.data_ptr()
-        desc.workspace_bytes = workspace.numel() * workspace.element_size()
+        workspace = alloc_workspace(desc, q.device, s)
+    desc.workspace = workspace.data_ptr()
+    desc.workspace_bytes = workspace.numel() * workspace.element_size()
     if events is not None:
         desc.ev_main_begin, desc.ev_main_end = events
-    s = stream if stream is not None else torch.cuda.current_stream(q.device)
     st = lib.specmoe_verify_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                  ctx_lens.data_ptr(), chunk_lens.data_ptr(), float(scale),
                                  out.data_ptr(), lse.data_ptr(), s.cuda_stream, ctypes.byref(desc))

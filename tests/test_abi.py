@@ -44,7 +44,7 @@ def test_status_codes_match_header(lib):
 
 
 def _desc(**kw):
-    base = dict(B=2, Hq=32, Hkv=8, D=128, C_max=5, S_max=2304, dtype=bd.SPECMOE_BF16, split_len=0)
+    base = dict(B=2, Hq=32, Hkv=8, D=128, C_max=5, S_max=2304, dtype=bd.SPECMOE_BF16, grid_blocks=0)
     base.update(kw)
     return bd.make_desc(**base)
 
@@ -65,9 +65,10 @@ def _call(lib, desc, q=FAKE, k=FAKE, v=FAKE, ctx=FAKE, chunk=FAKE, scale=0.088, 
     (dict(S_max=4, C_max=5), -2),
     (dict(Hq=30, Hkv=8), -3),
     (dict(C_max=17, Hq=32, Hkv=4), -6),          # 17 * 8 = 136 rows > 128
-    (dict(split_len=100), -7),                   # not a multiple of the key tile
-    (dict(split_len=-128), -7),
-    (dict(S_max=1 << 24), -2),                   # slab offsets would pass 2^31 bytes
+    (dict(grid_blocks=-1), -7),
+    (dict(grid_blocks=(1 << 20) + 1), -7),
+    (dict(S_max=1 << 23), -2),                   # slab offsets would pass 2^31 bytes
+    (dict(S_max=1 << 24, dtype=bd.SPECMOE_BF16, D=64), -2),   # packed lengths need T < 2^24
 ])
 def test_invalid_descriptor(lib, kw, code):
     assert _call(lib, _desc(**kw)) == code
@@ -76,6 +77,7 @@ def test_invalid_descriptor(lib, kw, code):
 
 def test_null_and_alignment_and_scale(lib):
     d = _desc()
+    d.workspace, d.workspace_bytes = FAKE, 1 << 30
     assert _call(lib, None) == -1
     for arg in ("q", "k", "v", "ctx", "chunk", "out", "lse"):
         assert _call(lib, d, **{arg: None}) == -1, arg
@@ -86,32 +88,37 @@ def test_null_and_alignment_and_scale(lib):
 
 
 def test_workspace_contract(lib):
-    d = _desc(B=64, split_len=512)             # 2304 / 512 -> 5 splits per unit
+    d = _desc(B=64, grid_blocks=512)
     need = lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d))
     rows = 5 * 4                                # C_max * g
-    slots = 64 * 8 * 5 * rows
-    assert need >= slots * (128 + 1) * 4
-    assert need < slots * (128 + 1) * 4 + 256
+    slots = 2 * 512 * rows                      # two partial pieces per workgroup
+    counters = 64 * 8 * 4
+    assert need >= counters + slots * (128 + 1) * 4
+    assert need < counters + slots * (128 + 1) * 4 + 512
+    # the workspace grows with the grid
+    d2 = _desc(B=64, grid_blocks=1024)
+    assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d2)) > need
+    # default grid = 512 workgroups
+    assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(_desc(B=64))) == need
     assert _call(lib, d) == -1                  # workspace needed but NULL
     d.workspace, d.workspace_bytes = FAKE, need - 1
     assert _call(lib, d) == -8
     d.workspace, d.workspace_bytes = FAKE + 8, need
     assert _call(lib, d) == -9
-    # one split per unit needs no workspace
-    d1 = _desc(B=64, split_len=2304)
-    assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d1)) == 0
+    # the counter-zeroing entry point validates before launching anything
+    init = lib.specmoe_verify_attn_workspace_init
+    assert init(None, need, None, ctypes.byref(_desc(B=64))) == -1
+    assert init(FAKE, need - 1, None, ctypes.byref(_desc(B=64))) == -8
+    assert init(FAKE + 4, need, None, ctypes.byref(_desc(B=64))) == -9
+    assert init(FAKE, need, None, ctypes.byref(_desc(B=64, D=80))) == -4
 
 
-def test_split_len_choice(lib):
-    d = _desc(B=64)
-    tile = lib.specmoe_verify_attn_key_tile(ctypes.byref(d))
-    assert tile == 128                          # 32 KB of bf16 D=128 rows
-    L = lib.specmoe_verify_attn_split_len(ctypes.byref(d))
-    assert L % tile == 0 and L >= 5
-    assert lib.specmoe_verify_attn_split_len(ctypes.byref(_desc(split_len=256))) == 256
-    assert lib.specmoe_verify_attn_split_len(ctypes.byref(_desc(D=80))) == -4
+def test_key_tile(lib):
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc())) == 128   # 32 KB of bf16 D=128 rows
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=64))) == 256
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=64))) == 128
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=128))) == 64
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=80))) == -4
 
 
 def test_empty_batch_is_a_no_op(lib):
