@@ -45,13 +45,24 @@ enum {
   SPECMOE_ERR_HEAD_DIM = -4,      /* D is not 64 or 128                               */
   SPECMOE_ERR_DTYPE = -5,         /* dtype is not a specmoe_dtype value               */
   SPECMOE_ERR_ROWS = -6,          /* C_max * (Hq / Hkv) > 128 query rows per KV head  */
-  SPECMOE_ERR_GRID = -7,          /* grid_blocks is negative, larger than 2^20, or so
+  SPECMOE_ERR_GRID = -7,          /* grid_blocks is negative, larger than 2048, or so
                                      large that partial results would pass 2 GB       */
   SPECMOE_ERR_WORKSPACE = -8,     /* workspace smaller than the size query returns    */
   SPECMOE_ERR_ALIGN = -9,         /* q, k_cache, v_cache, out or workspace is not
                                      16-byte aligned                                  */
   SPECMOE_ERR_SCALE = -10,        /* scale is not finite                              */
-  SPECMOE_ERR_LAUNCH = -11        /* HIP reported an error for a kernel launch        */
+  SPECMOE_ERR_LAUNCH = -11,       /* HIP reported an error for a kernel launch        */
+  SPECMOE_ERR_FLAGS = -12         /* unknown bits set in flags                        */
+};
+
+/* Bits of specmoe_verify_desc.flags. */
+enum {
+  /* No work stealing: the split of every unit into pieces, and so the
+   * floating-point result, is the same on every call.  Without it, idle
+   * workgroups take over tail chunks of slower ones, which balances the
+   * launch but lets the rounding of split units vary from call to call
+   * (within the kernel's error bound). */
+  SPECMOE_DETERMINISTIC = 1
 };
 
 /* Problem description.  Sizes are in elements unless stated otherwise. */
@@ -66,6 +77,7 @@ typedef struct specmoe_verify_desc {
   int32_t dtype;      /* specmoe_dtype of q, k_cache, v_cache                       */
   int32_t grid_blocks;  /* persistent workgroups that share the key tiles; 0 = the
                            library default (512: two per CU of an MI355X)          */
+  int32_t flags;        /* SPECMOE_* flag bits (0 = default)                      */
   void* workspace;          /* device; caller-allocated scratch, >= workspace_bytes,
                                whose counter region is zero (see below)             */
   size_t workspace_bytes;   /* size of workspace in bytes                           */
@@ -79,9 +91,11 @@ typedef struct specmoe_verify_desc {
  *
  * Work split: the keys of every (sequence, KV head) are cut into tiles, and
  * the tiles of all of them are divided evenly among `grid_blocks` persistent
- * workgroups.  A (sequence, KV head) whose tiles span several workgroups is
- * computed in pieces that are merged with log-sum-exp weights -- the
- * sequence-dimension KV partition of Section 5.2 -- through the workspace.
+ * workgroups; a workgroup that finishes early takes over tail tiles of slower
+ * ones (unless flags has SPECMOE_DETERMINISTIC).  A (sequence, KV head) whose
+ * tiles span several workgroups is computed in pieces that are merged with
+ * log-sum-exp weights -- the sequence-dimension KV partition of Section 5.2 --
+ * through the workspace.
  *
  * Arguments (all device pointers, C-contiguous, row-major):
  *   q          [B, C_max, Hq, D] dtype.  Row (b, i) holds the queries of draft
@@ -111,8 +125,8 @@ typedef struct specmoe_verify_desc {
  * synchronise with the host: the work is asynchronous on `stream`, and the
  * buffers must stay valid until it completes.  Calls are reentrant; calls
  * that may run concurrently need distinct workspaces.  The workspace's
- * counter region must be zero when the call starts (see
- * specmoe_verify_attn_workspace_bytes); the call leaves it zero.
+ * state region and tags must be zeroed once before its first call (see
+ * specmoe_verify_attn_workspace_bytes); every call leaves them ready for the next.
  *
  * Errors: all host-side checks run before any HIP call; on an error nothing
  * is enqueued and one of the SPECMOE_ERR_* codes is returned.  A launch
@@ -124,22 +138,26 @@ int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
                         const specmoe_verify_desc* desc);
 
 /* Bytes of device workspace specmoe_verify_attn needs for `desc` (its
- * grid_blocks included); 0 for an invalid descriptor.  The workspace holds
- * per-(sequence, KV head) arrival counters followed by the partial results of
- * pieces.  The counters must be zero when a call starts; every call that
- * completes leaves them zero again, so a workspace zeroed once (for instance
- * by specmoe_verify_attn_workspace_init) can be reused for any number of
- * calls with the same or a smaller descriptor. */
+ * grid_blocks included); 0 for an invalid descriptor.  The workspace starts
+ * with a state region -- per-(sequence, KV head) arrival counters, work-claim
+ * marks, a probe counter and a call generation -- followed by the partial
+ * results of pieces and their tags.  The state region and the tags must be
+ * zero before the first call; every call that completes leaves them ready
+ * for the next (each call tags its pieces with a new generation), so a
+ * workspace initialised once by specmoe_verify_attn_workspace_init can be
+ * reused for any number of calls with the same Hq, Hkv, D, C_max and dtype,
+ * any B, lengths, flags and grid_blocks, as long as it is large enough. */
 size_t specmoe_verify_attn_workspace_bytes(const specmoe_verify_desc* desc);
 
-/* Zero the counter region of `workspace` (device, workspace_bytes long) with
+/* Zero the state region and the piece tags of `workspace` (device,
+ * workspace_bytes long) with
  * a small kernel on `stream` (a hipStream_t; NULL: the null stream).  Status:
  * SPECMOE_OK, a descriptor error, SPECMOE_ERR_NULL_POINTER, SPECMOE_ERR_ALIGN,
  * SPECMOE_ERR_WORKSPACE if the buffer is too small, or SPECMOE_ERR_LAUNCH. */
 int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, void* stream,
                                        const specmoe_verify_desc* desc);
 
-/* Keys per tile for `desc`'s dtype and D (32 KB of K rows).  Negative status
+/* Keys per tile for `desc`'s dtype and D (16 KB of K rows).  Negative status
  * for an invalid dtype or D. */
 int32_t specmoe_verify_attn_key_tile(const specmoe_verify_desc* desc);
 

@@ -23,7 +23,9 @@ STATUS = {
     0: "SPECMOE_OK", -1: "SPECMOE_ERR_NULL_POINTER", -2: "SPECMOE_ERR_SHAPE", -3: "SPECMOE_ERR_GQA",
     -4: "SPECMOE_ERR_HEAD_DIM", -5: "SPECMOE_ERR_DTYPE", -6: "SPECMOE_ERR_ROWS", -7: "SPECMOE_ERR_GRID",
     -8: "SPECMOE_ERR_WORKSPACE", -9: "SPECMOE_ERR_ALIGN", -10: "SPECMOE_ERR_SCALE", -11: "SPECMOE_ERR_LAUNCH",
+    -12: "SPECMOE_ERR_FLAGS",
 }
+SPECMOE_DETERMINISTIC = 1
 
 
 class Desc(ctypes.Structure):
@@ -31,7 +33,7 @@ class Desc(ctypes.Structure):
     _fields_ = [
         ("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32), ("D", ctypes.c_int32),
         ("C_max", ctypes.c_int32), ("S_max", ctypes.c_int32), ("dtype", ctypes.c_int32),
-        ("grid_blocks", ctypes.c_int32),
+        ("grid_blocks", ctypes.c_int32), ("flags", ctypes.c_int32),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
         ("ev_main_begin", ctypes.c_void_p), ("ev_main_end", ctypes.c_void_p),
     ]
@@ -78,9 +80,9 @@ def status_str(status: int) -> str:
     return load_library().specmoe_status_str(status).decode()
 
 
-def make_desc(B, Hq, Hkv, D, C_max, S_max, dtype: int, grid_blocks: int = 0,
+def make_desc(B, Hq, Hkv, D, C_max, S_max, dtype: int, grid_blocks: int = 0, flags: int = 0,
               workspace: Optional[torch.Tensor] = None, events=None) -> Desc:
-    d = Desc(B, Hq, Hkv, D, C_max, S_max, dtype, grid_blocks, None, 0, None, None)
+    d = Desc(B, Hq, Hkv, D, C_max, S_max, dtype, grid_blocks, flags, None, 0, None, None)
     if workspace is not None:
         d.workspace = workspace.data_ptr()
         d.workspace_bytes = workspace.numel() * workspace.element_size()
@@ -140,7 +142,7 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
                 stream: Optional[torch.cuda.Stream] = None, events=None,
-                check_lengths: bool = False):
+                check_lengths: bool = False, deterministic: bool = False):
     """Chunked verification attention; see ``include/specmoe_verify.h``.
 
     q [B, C_max, Hq, D], k_cache / v_cache [B, Hkv, S_max, D] (bf16 or f32),
@@ -149,7 +151,8 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     ``alloc_workspace``) is reused across calls; without one, a fresh
     workspace is allocated and zeroed.  ``check_lengths`` copies the
     lengths to the host (a synchronisation) and checks the kernel's
-    preconditions; off by default.
+    preconditions; off by default.  ``deterministic`` turns work stealing
+    off, so that repeated calls give bitwise-identical results.
     """
     lib = load_library()
     B, C_max, Hq, D = q.shape
@@ -173,7 +176,8 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
         lse = torch.empty((B, C_max, Hq), dtype=torch.float32, device=q.device)
     _check(out, "out", (B, C_max, Hq, D), torch.float32)
     _check(lse, "lse", (B, C_max, Hq), torch.float32)
-    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks)
+    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks,
+                     SPECMOE_DETERMINISTIC if deterministic else 0)
     s = stream if stream is not None else torch.cuda.current_stream(q.device)
     if B == 0:
         return out, lse

@@ -66,7 +66,8 @@ def _call(lib, desc, q=FAKE, k=FAKE, v=FAKE, ctx=FAKE, chunk=FAKE, scale=0.088, 
     (dict(Hq=30, Hkv=8), -3),
     (dict(C_max=17, Hq=32, Hkv=4), -6),          # 17 * 8 = 136 rows > 128
     (dict(grid_blocks=-1), -7),
-    (dict(grid_blocks=(1 << 20) + 1), -7),
+    (dict(grid_blocks=2049), -7),
+    (dict(flags=2), -12),
     (dict(S_max=1 << 23), -2),                   # slab offsets would pass 2^31 bytes
     (dict(S_max=1 << 24, dtype=bd.SPECMOE_BF16, D=64), -2),   # packed lengths need T < 2^24
 ])
@@ -91,10 +92,11 @@ def test_workspace_contract(lib):
     d = _desc(B=64, grid_blocks=512)
     need = lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d))
     rows = 5 * 4                                # C_max * g
-    slots = 2 * 512 * rows                      # two partial pieces per workgroup
-    counters = 64 * 8 * 4
-    assert need >= counters + slots * (128 + 1) * 4
-    assert need < counters + slots * (128 + 1) * 4 + 512
+    slots = 10 * 512 * rows                     # up to ten pieces per workgroup
+    state = 256 + 2048 * 4 * 4 + 1024 * 8 * 4  # generation + probe counter, claim marks, unit counters
+    tags = 10 * 512 * 8
+    assert need >= state + tags + slots * (128 + 1) * 4
+    assert need < state + tags + slots * (128 + 1) * 4 + 1024
     # the workspace grows with the grid
     d2 = _desc(B=64, grid_blocks=1024)
     assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d2)) > need
@@ -114,10 +116,10 @@ def test_workspace_contract(lib):
 
 
 def test_key_tile(lib):
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc())) == 128   # 32 KB of bf16 D=128 rows
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=64))) == 256
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=64))) == 128
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=128))) == 64
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc())) == 64    # 16 KB of bf16 D=128 rows
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=64))) == 128
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=64))) == 64
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=128))) == 32
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=80))) == -4
 
 
