@@ -208,7 +208,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
                    "head_dim": w.D, "ctx_lens_sum": int(ctx.sum()), "chunk_lens_sum": tokens,
-                   "C_max": w.C_max, "S_max": w.S_max, "grid_blocks": args.grid_blocks or 512,
+                   "C_max": w.C_max, "S_max": w.S_max, "grid_blocks": args.grid_blocks or 256,
                    "input_sets": n_sets,
                    "parallelism": "single GPU"},
         "verified_tokens_per_s": round(tokens / t, 1),

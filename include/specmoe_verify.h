@@ -52,17 +52,7 @@ enum {
                                      16-byte aligned                                  */
   SPECMOE_ERR_SCALE = -10,        /* scale is not finite                              */
   SPECMOE_ERR_LAUNCH = -11,       /* HIP reported an error for a kernel launch        */
-  SPECMOE_ERR_FLAGS = -12         /* unknown bits set in flags                        */
-};
-
-/* Bits of specmoe_verify_desc.flags. */
-enum {
-  /* No work stealing: the split of every unit into pieces, and so the
-   * floating-point result, is the same on every call.  Without it, idle
-   * workgroups take over tail chunks of slower ones, which balances the
-   * launch but lets the rounding of split units vary from call to call
-   * (within the kernel's error bound). */
-  SPECMOE_DETERMINISTIC = 1
+  SPECMOE_ERR_FLAGS = -12         /* flags is not 0                                   */
 };
 
 /* Problem description.  Sizes are in elements unless stated otherwise. */
@@ -76,8 +66,8 @@ typedef struct specmoe_verify_desc {
   int32_t S_max;      /* token capacity of the KV cache per (sequence, KV head)     */
   int32_t dtype;      /* specmoe_dtype of q, k_cache, v_cache                       */
   int32_t grid_blocks;  /* persistent workgroups that share the key tiles; 0 = the
-                           library default (512: two per CU of an MI355X)          */
-  int32_t flags;        /* SPECMOE_* flag bits (0 = default)                      */
+                           library default (256: one per CU of an MI355X)          */
+  int32_t flags;        /* reserved, must be 0                                     */
   void* workspace;          /* device; caller-allocated scratch, >= workspace_bytes,
                                whose counter region is zero (see below)             */
   size_t workspace_bytes;   /* size of workspace in bytes                           */
@@ -90,12 +80,13 @@ typedef struct specmoe_verify_desc {
  * specmoe_verify_attn -- chunked verification attention (Section 5.1).
  *
  * Work split: the keys of every (sequence, KV head) are cut into tiles, and
- * the tiles of all of them are divided evenly among `grid_blocks` persistent
- * workgroups; a workgroup that finishes early takes over tail tiles of slower
- * ones (unless flags has SPECMOE_DETERMINISTIC).  A (sequence, KV head) whose
- * tiles span several workgroups is computed in pieces that are merged with
- * log-sum-exp weights -- the sequence-dimension KV partition of Section 5.2 --
- * through the workspace.
+ * the tiles of all of them are divided into `grid_blocks` equal contiguous
+ * ranges, one per persistent workgroup.  A (sequence, KV head) whose tiles
+ * span several ranges is computed in pieces that are merged with log-sum-exp
+ * weights -- the sequence-dimension KV partition of Section 5.2 -- through
+ * the workspace.  The split depends only on the lengths and grid_blocks, and
+ * pieces are merged in a fixed order, so repeated calls with the same inputs
+ * give bitwise-identical results.
  *
  * Arguments (all device pointers, C-contiguous, row-major):
  *   q          [B, C_max, Hq, D] dtype.  Row (b, i) holds the queries of draft
@@ -125,8 +116,8 @@ typedef struct specmoe_verify_desc {
  * synchronise with the host: the work is asynchronous on `stream`, and the
  * buffers must stay valid until it completes.  Calls are reentrant; calls
  * that may run concurrently need distinct workspaces.  The workspace's
- * state region and tags must be zeroed once before its first call (see
- * specmoe_verify_attn_workspace_bytes); every call leaves them ready for the next.
+ * counter region must be zeroed once before its first call (see
+ * specmoe_verify_attn_workspace_bytes); every call leaves it ready for the next.
  *
  * Errors: all host-side checks run before any HIP call; on an error nothing
  * is enqueued and one of the SPECMOE_ERR_* codes is returned.  A launch
@@ -139,18 +130,18 @@ int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
 
 /* Bytes of device workspace specmoe_verify_attn needs for `desc` (its
  * grid_blocks included); 0 for an invalid descriptor.  The workspace starts
- * with a state region -- per-(sequence, KV head) arrival counters, work-claim
- * marks, a probe counter and a call generation -- followed by the partial
- * results of pieces and their tags.  The state region and the tags must be
- * zero before the first call; every call that completes leaves them ready
- * for the next (each call tags its pieces with a new generation), so a
- * workspace initialised once by specmoe_verify_attn_workspace_init can be
- * reused for any number of calls with the same Hq, Hkv, D, C_max and dtype,
- * any B, lengths, flags and grid_blocks, as long as it is large enough. */
+ * with a counter region -- one arrival counter per (sequence, KV head) of a
+ * launch of up to 1024 sequences, at offsets that depend only on Hkv --
+ * followed by the partial results of pieces (two slots per workgroup).  The
+ * counter region must be zero before the first call; every call that
+ * completes leaves it zero again (the piece that merges a unit resets the
+ * unit's counter), so a workspace initialised once by
+ * specmoe_verify_attn_workspace_init can be reused for any number of calls
+ * with the same Hkv, any B, lengths and grid_blocks, as long as it is large
+ * enough for them. */
 size_t specmoe_verify_attn_workspace_bytes(const specmoe_verify_desc* desc);
 
-/* Zero the state region and the piece tags of `workspace` (device,
- * workspace_bytes long) with
+/* Zero the counter region of `workspace` (device, workspace_bytes long) with
  * a small kernel on `stream` (a hipStream_t; NULL: the null stream).  Status:
  * SPECMOE_OK, a descriptor error, SPECMOE_ERR_NULL_POINTER, SPECMOE_ERR_ALIGN,
  * SPECMOE_ERR_WORKSPACE if the buffer is too small, or SPECMOE_ERR_LAUNCH. */

@@ -25,7 +25,6 @@ STATUS = {
     -8: "SPECMOE_ERR_WORKSPACE", -9: "SPECMOE_ERR_ALIGN", -10: "SPECMOE_ERR_SCALE", -11: "SPECMOE_ERR_LAUNCH",
     -12: "SPECMOE_ERR_FLAGS",
 }
-SPECMOE_DETERMINISTIC = 1
 
 
 class Desc(ctypes.Structure):
@@ -142,7 +141,7 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
                 stream: Optional[torch.cuda.Stream] = None, events=None,
-                check_lengths: bool = False, deterministic: bool = False):
+                check_lengths: bool = False):
     """Chunked verification attention; see ``include/specmoe_verify.h``.
 
     q [B, C_max, Hq, D], k_cache / v_cache [B, Hkv, S_max, D] (bf16 or f32),
@@ -151,8 +150,8 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     ``alloc_workspace``) is reused across calls; without one, a fresh
     workspace is allocated and zeroed.  ``check_lengths`` copies the
     lengths to the host (a synchronisation) and checks the kernel's
-    preconditions; off by default.  ``deterministic`` turns work stealing
-    off, so that repeated calls give bitwise-identical results.
+    preconditions; off by default.  Repeated calls with the same inputs and
+    grid give bitwise-identical results.
     """
     lib = load_library()
     B, C_max, Hq, D = q.shape
@@ -176,8 +175,7 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
         lse = torch.empty((B, C_max, Hq), dtype=torch.float32, device=q.device)
     _check(out, "out", (B, C_max, Hq, D), torch.float32)
     _check(lse, "lse", (B, C_max, Hq), torch.float32)
-    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks,
-                     SPECMOE_DETERMINISTIC if deterministic else 0)
+    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks)
     s = stream if stream is not None else torch.cuda.current_stream(q.device)
     if B == 0:
         return out, lse

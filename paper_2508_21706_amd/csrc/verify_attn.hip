@@ -4,67 +4,82 @@
 // the cached context plus the draft chunk, with a chain mask inside the chunk
 // (SpecMoEOff, Section 5.1), and the log-sum-exp of every row.
 //
-// Design (one kernel launch per call):
+// Design (one kernel launch per call, one persistent workgroup per CU):
 //   * Unit of work = (sequence b, KV head).  The c_b draft tokens times the g
 //     query heads that share the KV head form the unit's R_b = c_b*g query
-//     rows; they are packed into 32-row MFMA tiles, so Q K^T and P V become
-//     small dense contractions that reuse every K/V byte for all rows.
-//   * Key tiles: a unit's keys [0, T_b) are cut into tiles of kTileKeys keys
+//     rows, cut into 16-row blocks, so that Q K^T and P V become small dense
+//     MFMA contractions that reuse every K/V byte for all rows.
+//   * Key tiles: a unit's keys [0, T_b) are cut into tiles of 16 KB of K rows
 //     anchored at T_b (tile n-1 = [T_b - kTileKeys, T_b)), so the chunk's own
-//     keys always sit in the unit's last tile and every tile holds a key that
-//     every query row of the unit can see.
+//     keys sit at the end of the unit's last tile.
 //   * Stream-K schedule: the tiles of all units, in unit order, form one list
-//     that is cut into equal contiguous ranges, one per persistent workgroup
-//     (2 per CU).  Every workgroup streams the same number of K/V bytes, so no
-//     CU idles at the end of the launch.  A unit cut by a range boundary is a
-//     sequence-wise KV partition whose partial results must be combined, as
-//     the paper notes for its sequence-dimension KV split (Section 5.2): each
-//     piece writes (O/l, lse) to the workspace, counts itself on an atomic
-//     arrival counter, and the last piece to arrive merges all of them with
-//     log-sum-exp weights.  Uncut units write their result directly.
-//   * K/V streaming: each iteration stages a 32 KB K tile and a 32 KB V tile
-//     in LDS with fully coalesced 16-byte loads (one wave instruction reads
-//     1 KB of contiguous cache rows); the next tile's loads are in flight in
-//     registers while the current tile is consumed.  LDS rows are padded by
-//     16 bytes, so every MFMA operand read is free of bank conflicts and all
-//     operand addresses are a per-lane base plus an immediate.
+//     cut into equal contiguous ranges, one per workgroup, so that every
+//     workgroup streams the same number of K/V bytes.  A unit cut by a range
+//     boundary is a sequence-wise KV partition whose partial results must be
+//     combined, as the paper notes for its sequence-dimension KV split
+//     (Section 5.2): each piece writes (O/l, lse) to the workspace and counts
+//     itself on an arrival counter; the last piece to arrive merges all of
+//     them with log-sum-exp weights.  A workgroup streams the cut unit at the
+//     end of its range first, so both pieces of every cut unit are done, and
+//     merged, early in the launch, while the memory pipeline keeps streaming.
+//   * Warp-specialised pipeline: 4 producer waves stream K/V tiles from HBM
+//     straight into a 4-stage LDS ring with direct-to-LDS loads (one wave
+//     instruction moves 1 KB of contiguous cache rows); three tiles (96 KB)
+//     are in flight while 8 consumer waves compute on the fourth.  Only the
+//     producers issue tile loads, so a consumer's wait for its own stores or
+//     loads never drains the tile stream.  LDS rows are padded by 16 bytes,
+//     so every MFMA operand read is free of bank conflicts and all operand
+//     addresses are a per-lane base plus an immediate.
 //   * Scores are formed transposed, S^T = K Q^T (keys on the MFMA M side,
-//     query rows on N), so each lane holds one query row: the online-softmax
-//     row statistics are per-lane scalars, row reductions need one cross-lane
-//     step (lanes l and l^32), and the probabilities are already in the B
-//     operand layout of O^T = V^T P^T.
-//   * bf16 inputs use v_mfma_f32_32x32x16_bf16 with fp32 accumulation (P is
-//     rounded to bf16 for the PV product); f32 inputs use v_mfma_f32_32x32x2_f32.
+//     query rows on N), so each lane holds one query row and four keys: row
+//     statistics need two cross-lane steps, and the probabilities are already
+//     the B operand of O^T = V^T P^T.  The consumers split a tile's 16-key
+//     blocks between them; their partial (max, sum, O) states are merged
+//     through LDS at the end of each unit.
+//   * bf16 inputs use v_mfma_f32_16x16x32_bf16 for the scores and
+//     v_mfma_f32_16x16x16_bf16 for P V, with fp32 accumulation (P is rounded
+//     to bf16 for the PV product); f32 inputs use v_mfma_f32_16x16x4_f32.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "specmoe_verify.h"
 
 namespace {
 
-constexpr int kThreads = 256;        // 4 waves of 64
-constexpr int kWaves = 4;
-constexpr int kSub = 32;             // keys per MFMA subtile
-constexpr int kRowTile = 32;         // query rows per MFMA tile
-constexpr int kMaxRows = 128;        // row tiles per unit <= 4
-constexpr int kTileBytes = 16384;    // K bytes (and V bytes) of one tile
-constexpr int kDefaultGrid = 512;    // persistent workgroups: 2 per CU on MI355X's 256 CUs
-constexpr int kMaxSeqs = 1024;       // sequences per launch (their lengths live in LDS)
+constexpr int kProducers = 4;                 // waves that stream K/V into LDS
+constexpr int kConsumers = 8;                 // waves that compute
+constexpr int kWaves = kProducers + kConsumers;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kCThreads = 64 * kConsumers;
+constexpr int kStages = 4;                    // LDS ring of staged tiles
+constexpr int kHalf = 16384;                  // K bytes (and V bytes) of one tile
+constexpr int kMaxDma = 5;                    // DMA instructions per producer wave and K (or V) tile, at most
+constexpr int kBlk = 16;                      // keys (and query rows) per MFMA block
+constexpr int kMaxRows = 128;                 // row blocks per unit <= 8
+constexpr int kDefaultGrid = 256;             // persistent workgroups: one per CU of an MI355X
+constexpr int kMaxGrid = 2048;
+constexpr int kMaxSeqs = 1024;                // sequences per launch (their lengths live in LDS)
 constexpr float kLog2e = 1.4426950408889634f;
+// The running max is only raised when a block's max exceeds it by more than
+// this (log2 units): probabilities stay <= 2^8, and the O rescale is skipped
+// for most blocks.
+constexpr float kLazyMax = 8.f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-typedef __attribute__((ext_vector_type(16))) float f32x16;
+
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(8))) short i16x8;
+typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 
-// Cache policy of the partial-result buffer accesses: device (agent) scope,
-// so the data goes through, or around, the XCD-local L2 to the point where
-// every XCD sees it, without an L2-wide write-back or invalidate.
+// Cache policy of the partial-result accesses: device (agent) scope, so the
+// data goes through, or around, the XCD-local L2 to the point where every XCD
+// sees it, without an L2-wide write-back or invalidate.
 constexpr int kDeviceCoherent = 16;   // SC1
 constexpr int kBufferFormat = 0x00020000;   // raw 32-bit buffer descriptor word 3
 
@@ -76,15 +91,10 @@ struct Params {
   const int32_t* chunk_lens;
   float* out;
   float* lse;
-  int* counters;    // [B*Hkv] per-unit tile counts of published pieces, zero between calls
-  int* claims;      // [P][4] tail-chunk claim marks
-  int* thief_ctr;   // steal probes of the current call, zero between calls
-  int* gen;         // generation: a call's claim/piece mark is gen + 1
-  float* ws_o;      // [slots][Rcap][D] normalised partial outputs
-  float* ws_lse;    // [slots][Rcap] partial log-sum-exp
-  int* ws_tag;      // [slots][2] (mark, unit) of the piece in each slot
-  int ws_o_bytes, ws_lse_bytes, ws_tag_bytes;
-  int deterministic;  // no stealing
+  int* counters;    // [B*Hkv] pieces arrived per unit, zero between calls
+  float* ws_o;      // [2P][Rcap][D] normalised partial outputs
+  float* ws_lse;    // [2P][Rcap] partial log-sum-exp
+  int ws_o_bytes, ws_lse_bytes;
   int B, Hq, Hkv, g, C_max, S_max;
   int Rcap;         // C_max * g
   int P;            // persistent workgroups
@@ -95,32 +105,50 @@ template <bool BF16, int D>
 struct Cfg {
   static constexpr int kElt = BF16 ? 2 : 4;
   static constexpr int kRowBytes = D * kElt;
-  static constexpr int kChunks = kRowBytes / 16;          // 16-byte chunks per row
-  static constexpr int kSlots = kChunks + 1;               // LDS slots per row: the chunks + one pad
-  static constexpr int kPitch = 16 * kSlots;               // padded LDS row pitch
-  static constexpr int kTileKeys = kTileBytes / kRowBytes;
-  static constexpr int kLdsTile = kTileKeys * kPitch;      // LDS bytes of one staged K (or V) tile
-  static constexpr int kInst = (kTileKeys * kSlots + 63) / 64;   // 64-slot DMA instructions per tile
-  static constexpr int kNSub = kTileKeys / kSub;
-  static constexpr int kQChunks = kChunks / 2;             // Q chunks held per lane
-  static constexpr int kDC = D / 32;                       // 32-wide d blocks of O^T
+  static constexpr int kChunks = kRowBytes / 16;           // 16-byte chunks per row
+  static constexpr int kTileKeys = kHalf / kRowBytes;
+  static constexpr int kSlots = kChunks + 1;                // LDS slots per row: the chunks and one pad
+  static constexpr int kPitch = 16 * kSlots;                // padded LDS row pitch
+  static constexpr int kLdsHalf = kTileKeys * kPitch;       // LDS bytes of a staged K (or V) tile
+  static constexpr int kStage = 2 * kLdsHalf;
+  static constexpr int kInst = (kTileKeys * kSlots + 63) / 64;   // 64-slot DMA instructions per K (or V) tile
+  static constexpr int kNKB = kTileKeys / kBlk;             // 16-key blocks per tile
+  static constexpr int kDB = D / 16;                        // 16-wide d blocks of O^T
+  static constexpr int kQJ = kChunks / 4;                   // 16-byte Q chunks per lane
+  static_assert(kInst <= 4 * kMaxDma && kInst >= 16 && kInst <= 18, "producer wait counts assume 16..18 DMA instructions");
+  static_assert(kStages * kStage + 12 * 1024 <= 160 * 1024, "LDS budget");
+  static_assert(4 * 64 * D <= kStage, "key-split merge scratch fits in a stage");
 };
 
-// Byte offset of 16-byte chunk `c` of row `row` inside a staged LDS tile.  The
-// 16-byte row padding shifts consecutive rows by four banks, so 16 lanes that
-// read the same chunk of 16 consecutive rows hit 64 distinct banks.
-template <class C>
-__device__ __forceinline__ int lds_off(int row, int c) {
-  return row * C::kPitch + 16 * c;
+// Workgroup barrier that waits only for this wave's LDS operations.  A
+// __syncthreads() also waits for every outstanding direct-to-LDS load (its
+// release fence covers them), which would drain the tile pipeline at every
+// barrier; tile data is handed over by the producers' explicit waits instead.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
+// Max and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 that hold one
+// query row, with the gfx950 lane-swap instructions (no LDS round trip).
+// Every lane combines the same two operands in the same order, so all four
+// get bitwise-equal results.
+__device__ __forceinline__ float row_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float row_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   __bf16 a = (__bf16)lo;
   __bf16 b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) |
-         ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
 // Lengths of sequence b, clamped into the documented ranges so that no access
@@ -135,100 +163,76 @@ __device__ __forceinline__ uint32_t load_seq(const Params& p, int b) {
   return ((uint32_t)(l + c) << 8) | (uint32_t)c;
 }
 __device__ __forceinline__ int seq_T(uint32_t s) { return (int)(s >> 8); }
+// a value every lane of the wave holds, moved to a scalar register
+__device__ __forceinline__ int uniform(int x) { return __builtin_amdgcn_readfirstlane(x); }
+__device__ __forceinline__ uint32_t uniform(uint32_t x) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)x); }
 __device__ __forceinline__ int seq_c(uint32_t s) { return (int)(s & 0xffu); }
 template <class C>
 __device__ __forceinline__ int seq_tiles(uint32_t s) {
   return seq_c(s) == 0 ? 0 : (seq_T(s) + C::kTileKeys - 1) / C::kTileKeys;
 }
 
-// Tile schedule shared by every workgroup of a launch.  The tiles of all
-// units form one list [0, N) cut into Pe equal contiguous home ranges (one
-// per workgroup).  The last ~quarter of each range is cut into nt tail
-// chunks of cs tiles that other workgroups may steal; the rest is the head.
+// Tile schedule shared by every workgroup of a launch: the tiles of all units
+// form one list [0, N), cut into Pe equal contiguous ranges.
 struct Sched {
-  int N, Pe, nt, cs;
+  int N, Pe;
   __device__ int range_begin(int q) const { return (int)((long long)q * N / Pe); }
-  // home range holding tile t
-  __device__ int range_owner(int t) const { return (int)(((long long)(t + 1) * Pe - 1) / N); }
-  __device__ int head_end(int q) const { return range_begin(q + 1) - nt * cs; }
-  // sub-range x of range q: x = 0 is the head, x = 1 + i tail chunk i
-  __device__ int sub_begin(int q, int x) const { return x == 0 ? range_begin(q) : head_end(q) + (x - 1) * cs; }
-  __device__ int sub_end(int q, int x) const { return x == 0 ? head_end(q) : head_end(q) + x * cs; }
-  __device__ int sub_index(int t) const {
-    const int q = range_owner(t);
-    const int h = head_end(q);
-    return q * (nt + 1) + (t < h ? 0 : 1 + (t - h) / cs);
-  }
+  __device__ int owner(int t) const { return (int)(((long long)(t + 1) * Pe - 1) / N); }
 };
 
-// Merge every published piece of a unit; run by all threads of the
-// workgroup whose piece completed the unit's tile count.  A piece sits in
-// slot 2*x + side of the sub-range x where it starts and is tagged
-// (mark, unit); the candidates are both slots of every sub-range that meets
-// the unit, taken in a fixed order.  Inlined: a call would make the
-// streaming loop keep its live registers across the call boundary.
+// Position of a tile: sequence, KV head, tile index inside the unit, and the
+// sequence's packed lengths.
+struct Cursor {
+  int b, kvh, j;
+  uint32_t s;
+};
+
+// Merge every piece of a unit; run by the consumer threads of the workgroup
+// whose piece arrived last.  Range q's piece of the unit is its first
+// segment (slot 2q), except when range q starts before the unit: then it is
+// q's last segment (slot 2q+1).
 template <int D>
-__device__ __forceinline__ void merge_unit(const Params& p, const Sched& sc, const uint32_t* seqs, char* lds,
-                                        int mark, int unit, int unit_first, int n_unit) {
-  const int tid = threadIdx.x;
-  const int g = p.g, Hkv = p.Hkv;
+__device__ __forceinline__ void merge_unit(const Params& p, const Sched& sc, const uint32_t* seqs, int ctid,
+                                        int unit, int unit_first, int n_unit) {
   const __amdgpu_buffer_rsrc_t ws_o_rsrc = __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
   const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
-  const __amdgpu_buffer_rsrc_t ws_tag_rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(p.ws_tag, 0, p.ws_tag_bytes, kBufferFormat);
-  const int unit_last = unit_first + n_unit - 1;
-  const int qf = sc.range_owner(unit_first);
-  const int ql = sc.range_owner(unit_last);
-  const int per_q = 2 * (sc.nt + 1);
-  const int ncand = (ql - qf + 1) * per_q;
-  unsigned char* valid = reinterpret_cast<unsigned char*>(lds);
-  __syncthreads();   // the LDS tile is free: every wave is past its compute
-  for (int c = tid; c < ncand; c += kThreads) {
-    const int q = qf + c / per_q;
-    const int x = (c % per_q) >> 1;
-    const int slot = 2 * (q * (sc.nt + 1) + x) + (c & 1);
-    bool ok = sc.sub_begin(q, x) <= unit_last && sc.sub_end(q, x) > unit_first;
-    if (ok) {
-      const int tm = __builtin_amdgcn_raw_buffer_load_b32(ws_tag_rsrc, slot * 8, 0, kDeviceCoherent);
-      const int tu = __builtin_amdgcn_raw_buffer_load_b32(ws_tag_rsrc, slot * 8 + 4, 0, kDeviceCoherent);
-      ok = tm == mark && tu == unit;
-    }
-    valid[c] = ok ? 1 : 0;
-  }
-  __syncthreads();
-  const int ub = unit / Hkv;
-  const int ukvh = unit - ub * Hkv;
-  const int uR = seq_c(seqs[ub]) * g;
+  const int qf = sc.owner(unit_first);
+  const int ql = sc.owner(unit_first + n_unit - 1);
+  const int slot_first = 2 * qf + (sc.range_begin(qf) < unit_first ? 1 : 0);
+  const int ub = unit / p.Hkv;
+  const int ukvh = unit - ub * p.Hkv;
+  const int g = p.g;
+  const int uR = seq_c(uniform(seqs[ub])) * g;
   constexpr int kBatch = 4;
-  for (int idx = tid; idx < uR * (D / 4); idx += kThreads) {
+  for (int idx = ctid; idx < uR * (D / 4); idx += kCThreads) {
     const int r = idx / (D / 4);
     const int d0 = 4 * (idx - r * (D / 4));
     float m = -INFINITY, z = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    int c = 0;
-    while (c < ncand) {
+    for (int q0 = qf; q0 <= ql; q0 += kBatch) {
       float lq[kBatch];
-      f32x4 xv[kBatch];
-      int got = 0;
-      // gather up to kBatch valid pieces, then fold them in
-      for (; c < ncand && got < kBatch; ++c) {
-        if (!valid[c]) continue;
-        const int q = qf + c / per_q;
-        const int x = (c % per_q) >> 1;
-        const int srow = (2 * (q * (sc.nt + 1) + x) + (c & 1)) * p.Rcap + r;
-        lq[got] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ws_lse_rsrc, srow * 4, 0,
+      f32x4 x[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int q = q0 + u;
+        const int srow = (q == qf ? slot_first : 2 * q) * p.Rcap + r;
+        if (q <= ql) {
+          lq[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ws_lse_rsrc, srow * 4, 0,
+                                                                               kDeviceCoherent));
+          x[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ws_o_rsrc, (srow * D + d0) * 4, 0,
                                                                                 kDeviceCoherent));
-        xv[got] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                ws_o_rsrc, (srow * D + d0) * 4, 0, kDeviceCoherent));
-        ++got;
+        }
       }
-      for (int u = 0; u < got; ++u) {
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (q0 + u > ql) break;
+        if (lq[u] == -INFINITY) continue;   // a piece in which this row sees no key
         const float nm = fmaxf(m, lq[u]);
         const float a = expf(m - nm);
         const float w = expf(lq[u] - nm);
         z = z * a + w;
-        acc = acc * a + w * xv[u];
+        acc = acc * a + w * x[u];
         m = nm;
       }
     }
@@ -236,26 +240,29 @@ __device__ __forceinline__ void merge_unit(const Params& p, const Sched& sc, con
     *reinterpret_cast<f32x4*>(p.out + orow * D + d0) = acc * (1.f / z);
     if (d0 == 0) p.lse[orow] = m + logf(z);
   }
-  if (tid == 0)   // ready for the next call
+  if (ctid == 0)   // ready for the next call
     __hip_atomic_store(p.counters + unit, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <bool BF16, int D>
-__global__ __launch_bounds__(kThreads, 2) void verify_attn_kernel(Params p) {
+__global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   using C = Cfg<BF16, D>;
-  // two tile buffers, each a K tile followed by a V tile
-  __shared__ __attribute__((aligned(16))) char smem[2 * 2 * C::kLdsTile];
+  __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
   __shared__ uint32_t seqs[kMaxSeqs];     // packed (T, c) of every sequence of the launch
   __shared__ int pref[kMaxSeqs + 1];      // tiles per KV head of the sequences before b
+  __shared__ float mst[4][2][64];         // key-split merge: running max and partial sums
   __shared__ int wave_sum[kWaves];
-  __shared__ int sh_int[4];               // broadcast slots: mark, claim result, flag, probe result
+  __shared__ int sh_flag[2];              // "the counted piece completed its unit", by iteration parity
 
   const int pid = blockIdx.x;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int lr = lane & 31;     // row (or key, or d) index inside a 32-wide MFMA block
-  const int half = lane >> 5;   // which half of the MFMA k dimension this lane feeds
+  const int wave = uniform(tid >> 6);
+  const bool producer = wave < kProducers;
+  const int wc = wave - kProducers;       // consumer wave index
+  const int ctid = tid - 64 * kProducers; // consumer thread index
+  const int lm = lane & 15;               // row (or key, or d) inside a 16-wide MFMA block
+  const int lg = lane >> 4;               // which quarter of the MFMA k dimension this lane feeds
   const int B = p.B, Hkv = p.Hkv, g = p.g;
 
   // ---- prologue: lengths and tile prefix sums into LDS (block-wide scan).
@@ -276,7 +283,6 @@ __global__ __launch_bounds__(kThreads, 2) void verify_attn_kernel(Params p) {
     if (lane >= off) incl += y;
   }
   if (lane == 63) wave_sum[wave] = incl;
-  if (tid == 0) sh_int[0] = 1 + __hip_atomic_load(p.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
   int before = 0, total = 0;
 #pragma unroll
@@ -284,6 +290,7 @@ __global__ __launch_bounds__(kThreads, 2) void verify_attn_kernel(Params p) {
     before += w < wave ? wave_sum[w] : 0;
     total += wave_sum[w];
   }
+  total = uniform(total);
   {
     int run = incl - my_tiles + before;
     for (int b = b_lo; b < b_hi; ++b) {
@@ -292,24 +299,9 @@ __global__ __launch_bounds__(kThreads, 2) void verify_attn_kernel(Params p) {
     }
     if (tid == kThreads - 1) pref[B] = total;
   }
-  const int mark = sh_int[0];   // this call's claim / piece mark (generation + 1)
   Sched sc;
   sc.N = total * Hkv;           // tiles of all units (< 2^31, host check)
-  // workgroups that get tiles: at most one per tile, so no home range is empty
-  sc.Pe = sc.N < p.P ? sc.N : p.P;
-  {
-    const int S = sc.Pe > 0 ? sc.N / sc.Pe : 0;
-    if (p.deterministic || S < 8) {
-      sc.nt = 0;
-      sc.cs = 1;
-    } else {
-      // chunks of at least 2 tiles: the owner claims a chunk two tiles
-      // before it would stream it, so the claim is settled in time
-      const int tail = S / 4;
-      sc.cs = max(2, (tail + 3) / 4);
-      sc.nt = min(4, tail / sc.cs);
-    }
-  }
+  sc.Pe = sc.N < p.P ? sc.N : p.P;   // at most one workgroup per tile: no range is empty
   __syncthreads();
 
   // ---- padding rows c_b <= i < C_max of the sequences b = pid (mod P):
@@ -329,9 +321,9 @@ __global__ __launch_bounds__(kThreads, 2) void verify_attn_kernel(Params p) {
   }
   if (pid >= sc.Pe) return;
 
-  // (b, kv head, tile) of global tile t: a 64-ary search of the prefix sums
-  // done by every wave on its own (two LDS reads and two ballots).
-  auto locate = [&](int t, int& ob, int& okvh, int& oj) {
+  // Cursor of global tile t: a 64-ary search of the prefix sums, done by
+  // every wave on its own (two LDS reads and two ballots).
+  auto locate = [&](int t) {
     const int tq = t / Hkv;                      // tiles per KV head before t's sequence, at most
     const int step = (B + 64) / 64;              // B + 1 prefix entries in 64 groups
     const int i1 = min(lane * step, B);
@@ -339,484 +331,503 @@ __global__ __launch_bounds__(kThreads, 2) void verify_attn_kernel(Params p) {
     const int base = (63 - __builtin_clzll(m1)) * step;
     const int i2 = min(base + lane, B);
     const unsigned long long m2 = __ballot(lane < step && pref[i2] <= tq);
-    const int b = base + 63 - __builtin_clzll(m2);
-    const int n = seq_tiles<C>(seqs[b]);
-    const int off = t - Hkv * pref[b];
-    ob = b;
-    okvh = off / n;
-    oj = off - okvh * n;
+    Cursor cu;
+    cu.b = uniform(base + 63 - __builtin_clzll(m2));
+    cu.s = uniform(seqs[cu.b]);
+    const int n = seq_tiles<C>(cu.s);
+    const int off = t - Hkv * uniform(pref[cu.b]);
+    cu.kvh = off / n;
+    cu.j = off - cu.kvh * n;
+    return cu;
+  };
+  // global index of tile 0 of unit (b, kvh), and the unit's tile count
+  auto unit_tiles = [&](int unit, int& first_tile, int& n) {
+    const int b = unit / Hkv;
+    const int kvh = unit - b * Hkv;
+    n = seq_tiles<C>(uniform(seqs[b]));
+    first_tile = Hkv * uniform(pref[b]) + kvh * n;
   };
 
-  // K/V tile (b, kvh, j) straight from HBM into LDS buffer `buf`.  Each
-  // 64-lane DMA instruction fills 64 consecutive 16-byte LDS slots, i.e.
-  // 1 KB of consecutive cache rows with their pad slots; a pad lane re-reads
-  // a chunk of its own row and rows past the end of a partial tile re-read
-  // the tile's last row, so every slot holds finite data from the same
-  // cache lines.  Wave w issues instructions w, w + 4, ...
-  auto dma_tile = [&](int buf, int b, int kvh, int j, uint32_t s, int n) {
-    const int T = seq_T(s);
-    const int hi = T - (n - 1 - j) * C::kTileKeys;
+  // ---- this workgroup's range [g0, g1).  If its last tile lies in a unit
+  // that starts inside the range and continues past it, that last segment
+  // [s_last, g1) is streamed first, then [g0, s_last).
+  const int g0 = sc.range_begin(pid);
+  const int g1 = sc.range_begin(pid + 1);
+  const int count = g1 - g0;
+  Cursor first = locate(g1 - 1);
+  const int s_last = g1 - 1 - first.j;
+  const bool rotated = s_last > g0 && first.j < seq_tiles<C>(first.s) - 1;
+  const int nL = rotated ? g1 - s_last : 0;    // tiles of the rotated segment
+  if (rotated) first.j = 0;
+  else first = locate(g0);
+  // global index of the tile at position v of the workgroup's order
+  auto tile_at = [&](int v) { return v < nL ? s_last + v : g0 + (v - nL); };
+  // the first tile of unit (b, kvh) after cursor cu's unit
+  auto next_unit = [&](Cursor& cu) {
+    cu.j = 0;
+    if (++cu.kvh == Hkv) {
+      cu.kvh = 0;
+      do {
+        ++cu.b;
+      } while (seq_tiles<C>(uniform(seqs[cu.b])) == 0);   // in range: the next tile exists
+      cu.s = uniform(seqs[cu.b]);
+    }
+  };
+  // the tile after position v (in the workgroup's order) of cursor cu
+  auto advance = [&](Cursor& cu, int v) {
+    if (v + 1 == nL) cu = locate(g0);   // end of the rotated segment
+    else if (++cu.j == seq_tiles<C>(cu.s)) next_unit(cu);
+  };
+  // the first tile of the segment after the one cu is in (cu at position v)
+  auto next_segment = [&](const Cursor& cu, int v, int& v_next) {
+    const int part_end = v < nL ? nL : count;
+    v_next = min(v + seq_tiles<C>(cu.s) - cu.j, part_end);
+    Cursor nx = cu;
+    if (v_next < count) {
+      if (v_next == nL) nx = locate(g0);
+      else next_unit(nx);
+    }
+    return nx;
+  };
+
+  // ---- producers: K/V tile of cursor cu straight from HBM into stage st.
+  // Each 64-lane load fills 64 consecutive 16-byte LDS slots (1 KB of
+  // consecutive cache rows with their pad slots); a pad lane re-reads a chunk
+  // of its own row, and rows past the end of a partial tile re-read the
+  // tile's last row, so every slot holds finite data from cache lines the
+  // tile reads anyway.  Producer wave w issues the K and V instructions
+  // w, w + 4, ...
+  int drow[kMaxDma], dch[kMaxDma];
+#pragma unroll
+  for (int k = 0; k < kMaxDma; ++k) {
+    const int sl = 64 * (wave + kProducers * k) + lane;
+    drow[k] = sl / C::kSlots;
+    dch[k] = min(sl % C::kSlots, C::kChunks - 1);
+  }
+  auto dma = [&](const Cursor& cu, int st) {
+    const int T = seq_T(cu.s);
+    const int hi = T - (seq_tiles<C>(cu.s) - 1 - cu.j) * C::kTileKeys;
     const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
     const int last = hi - lo - 1;
     // K/V slab of the unit; byte offsets inside it fit in 32 bits (host check)
-    const size_t slab = ((size_t)b * Hkv + kvh) * (size_t)p.S_max * C::kRowBytes;
+    const size_t slab = ((size_t)cu.b * Hkv + cu.kvh) * (size_t)p.S_max * C::kRowBytes;
     const char* kp = p.k + slab + (size_t)lo * C::kRowBytes;
     const char* vp = p.v + slab + (size_t)lo * C::kRowBytes;
-    char* kl = smem + buf * 2 * C::kLdsTile;
-    char* vl = kl + C::kLdsTile;
+    char* kl = smem + st * C::kStage;
+    char* vl = kl + C::kLdsHalf;
 #pragma unroll
-    for (int i = wave; i < C::kInst; i += kWaves) {
-      const int sl = 64 * i + lane;
-      const int row = sl / C::kSlots;
-      const int ch = sl - row * C::kSlots;
-      const uint32_t off = (uint32_t)min(row, last) * C::kRowBytes + 16u * min(ch, C::kChunks - 1);
-      if (sl < C::kTileKeys * C::kSlots) {
-        __builtin_amdgcn_global_load_lds(kp + off, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(vp + off, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0, 0);
+    for (int k = 0; k < kMaxDma; ++k) {
+      const int i = wave + kProducers * k;
+      if (i < C::kInst) {
+        const uint32_t off = (uint32_t)min(drow[k], last) * C::kRowBytes + 16u * dch[k];
+        if (64 * i + lane < C::kTileKeys * C::kSlots) {
+          __builtin_amdgcn_global_load_lds(kp + off, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
+                                           0);
+          __builtin_amdgcn_global_load_lds(vp + off, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0,
+                                           0);
+        }
       }
     }
   };
+  // wait until this producer's loads of a tile have landed in LDS, with
+  // `later` tiles issued after it still in flight (loads complete in order)
+  const int per_tile = 2 * ((C::kInst - wave + kProducers - 1) / kProducers);   // 8 or 10
+  auto wait_tile = [&](int later) {
+    switch (later * per_tile) {
+      case 20: asm volatile("s_waitcnt vmcnt(20)" ::: "memory"); break;
+      case 16: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+      case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+      case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+      default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    }
+  };
 
-  // per-segment state
-  u32x4 qreg[C::kQChunks];
-  f32x16 o[C::kDC];
-  float m_run = 0.f, l_run = 0.f;
-  int n_rt4 = 1, n_kg = 1, n_dh = 1, rt = 0, kg = 0, dh = 0, R = 0, row = 0, tok = 0, vis = 0, l_ctx = 0;
-  bool has_rows = false, row_valid = false;
-
-  // Wave roles and Q operand of the unit (b, kvh) with packed lengths s.
-  // The 4 waves split into row tiles x key groups x halves of D.
-  auto start_unit = [&](int b, int kvh, uint32_t s) {
-    const int c = seq_c(s);
+  // ---- consumer roles for the unit of cursor cu.  Rows are cut into
+  // n_rb 16-row blocks (n_rbp = n_rb rounded up to a power of two); consumer
+  // wave wc takes row block rb = wc % n_rbp and the key blocks
+  // kslot, kslot + kw, ... of every tile, kw = 8 / n_rbp.
+  int R = 0, n_rbp = 1, kw = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
+  bool active = false, row_valid = false;
+  auto roles = [&](const Cursor& cu) {
+    const int c = seq_c(cu.s);
     R = c * g;
-    l_ctx = seq_T(s) - c;
-    const int n_rt = (R + kRowTile - 1) / kRowTile;
-    n_rt4 = n_rt == 3 ? 4 : n_rt;
-    n_kg = min(kWaves / n_rt4, C::kNSub);
-    n_dh = kWaves / (n_rt4 * n_kg);
-    rt = wave % n_rt4;
-    kg = (wave / n_rt4) % n_kg;
-    dh = wave / (n_rt4 * n_kg);
-    has_rows = rt < n_rt;
-    row = rt * kRowTile + lr;
-    row_valid = has_rows && row < R;
+    l_ctx = seq_T(cu.s) - c;
+    const int n_rb = (R + kBlk - 1) / kBlk;
+    n_rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : n_rb <= 4 ? 4 : 8;
+    kw = kConsumers / n_rbp;
+    nks = min(kw, C::kNKB);                   // consumers that share a row block
+    rb = producer ? 0 : wc % n_rbp;
+    kslot = producer ? kw : wc / n_rbp;
+    active = !producer && rb < n_rb && kslot < nks;
+    row = rb * kBlk + lm;
+    row_valid = active && row < R;
     tok = row_valid ? row / g : 0;
     vis = row_valid ? l_ctx + tok : 0x7fffffff;   // last visible key of this lane's row
-    const char* qrow = p.q + ((size_t)(b * p.C_max + tok) * p.Hq + kvh * g + (row_valid ? row % g : 0)) *
-                                 C::kRowBytes;
+  };
+  // Q chunks of this lane's row for the unit of cu (zero for invalid rows):
+  // chunk 4J + lg of the row feeds the J-th score MFMA.  Consumers only.
+  auto load_q = [&](const Cursor& cu, u32x4* dst) {
+    const int c = seq_c(cu.s);
+    const int uR = c * g;
+    const int n_rb = (uR + kBlk - 1) / kBlk;
+    const int rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : n_rb <= 4 ? 4 : 8;
+    const int rb_ = wc % rbp;
+    const int ks_ = wc / rbp;
+    const int row_ = rb_ * kBlk + lm;
+    const bool ok = rb_ < n_rb && ks_ < min(kConsumers / rbp, C::kNKB) && row_ < uR;
+    const int tk = ok ? row_ / g : 0;
+    const char* qrow =
+        p.q + ((size_t)(cu.b * p.C_max + tk) * p.Hq + cu.kvh * g + (ok ? row_ % g : 0)) * C::kRowBytes;
 #pragma unroll
-    for (int j2 = 0; j2 < C::kQChunks; ++j2)
-      qreg[j2] = row_valid ? *reinterpret_cast<const u32x4*>(qrow + 16 * (2 * j2 + half))
-                           : u32x4{0u, 0u, 0u, 0u};
+    for (int J = 0; J < C::kQJ; ++J)
+      dst[J] = ok ? *reinterpret_cast<const u32x4*>(qrow + 16 * (4 * J + lg)) : u32x4{0u, 0u, 0u, 0u};
   };
 
-  // Partial results go through raw buffer descriptors so that they can use
-  // the device-coherent cache policy at 16-byte width.
-  const __amdgpu_buffer_rsrc_t ws_o_rsrc = __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
-  const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
-  const __amdgpu_buffer_rsrc_t ws_tag_rsrc =
-      __builtin_amdgcn_make_buffer_rsrc(p.ws_tag, 0, p.ws_tag_bytes, kBufferFormat);
-
-  // Publication of a piece: its device-coherent stores are issued at the end
-  // of its segment; the wait for every outstanding memory operation at the
-  // top of the next tile covers them, and the piece's tiles are then added to
-  // its unit's count.  The count comes back during that tile's compute; the
-  // piece that completes the count merges the unit.
-  bool pub_pending = false;
-  int pub_unit = 0, pub_first = 0, pub_n = 0, pub_tiles = 0;
-  auto count_piece = [&]() -> int {
-    int old = 0;
-    if (tid == 0)
-      old = __hip_atomic_fetch_add(p.counters + pub_unit, pub_tiles, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return old + pub_tiles == pub_n ? 1 : 0;
-  };
-  // wait for every outstanding vector-memory operation of this thread (tile
-  // DMA, Q loads, piece stores); the compiler fences keep it in place
-  auto wait_all = [&]() {
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_waitcnt(0);
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  // Publication of pieces (at most two per workgroup: its first and last
+  // segment).  The consumers' piece stores are acknowledged two iterations
+  // later (their own wait, which no tile load shares), the piece is then
+  // counted, and the count is read back one iteration after that; at most one
+  // piece is counted per iteration.  The loop runs idle iterations after the
+  // last tile until every piece is done.
+  struct Pub {
+    int state;   // 0 stored, 1 counted, 2 done
+    int unit, v;
+    int old;     // counter value before this piece (consumer thread 0)
   };
 
-  // Claim tail chunk i of home range q for this call (owner or thief).
-  auto claim = [&](int q, int i) -> int {
-    const int old = __hip_atomic_fetch_max(p.claims + q * 4 + i, mark, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return old < mark ? 1 : 0;
-  };
+  // ---- the main loop, instantiated once for the producers and once for the
+  // consumers.  The two roles share no control flow, so the compiler's
+  // memory-wait analysis of one role adds no wait to the other; both follow
+  // the same schedule and bookkeeping, so they meet at the same barriers.
+  auto run = [&](auto role) {
+    constexpr bool kProducer = decltype(role)::value;
+    // per-segment state of a consumer lane: O^T blocks, running max (log2
+    // units, the same in the four lanes of a row), this lane's share of the
+    // row sum, and the Q operand of this unit and of the next
+    f32x4 o[C::kDB];
+    u32x4 qr[C::kQJ], qn[C::kQJ];
+#pragma unroll
+    for (int J = 0; J < C::kQJ; ++J) qn[J] = u32x4{0u, 0u, 0u, 0u};
+    float m_run = -INFINITY, l_lane = 0.f;
+    Pub pub0 = {2, 0, 0, 0}, pub1 = {2, 0, 0, 0};
+    int n_pub = 0;
 
-  // ---- runs: the head of the home range, extended by the owner's tail
-  // chunks as long as it wins their claims; then stolen chunks.
-  const int g0 = sc.range_begin(pid);
-  const int h0 = sc.head_end(pid);
-  int run_a = g0, run_e = h0;
-  bool owner = true;
-  int ext = 0;        // tail chunks added to the owner's run
-  int issued = 0;     // tail-chunk claims issued by the owner
-  int claim_tile = sc.nt > 0 ? max(g0, h0 - 2) : -1;   // tile during which claim `issued` goes out
-  int claim_res = 0;
-  if (sc.nt > 0 && h0 - 2 < g0) {
-    // a one-tile head: claim chunk 0 before streaming
-    if (tid == 0) sh_int[1] = claim(pid, 0);
-    issued = 1;
-    claim_tile = -1;
-  }
+    // start: the first tiles in flight, the first unit's Q
+    Cursor dcur = first;                 // cursor of the next tile to load
+    int dv = 0;                          // its position in the workgroup's order
+    if constexpr (kProducer) {
+      for (; dv < kStages - 1 && dv < count; ++dv) {
+        dma(dcur, dv);
+        if (dv + 1 < count) advance(dcur, dv);
+      }
+    } else {
+      // through qn, so that qr is only ever written from registers and the
+      // score MFMAs never wait for a load
+      load_q(first, qn);
+#pragma unroll
+      for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
+    }
+    Cursor cur = first;                  // cursor of the tile being computed
+    int seg_g = g0;
 
-  for (;;) {
-    int cb, ckvh, cj;
-    locate(run_a, cb, ckvh, cj);
-    uint32_t cs = seqs[cb];
-    int cn = seq_tiles<C>(cs);
-    __syncthreads();           // both tile buffers are free
-    dma_tile(0, cb, ckvh, cj, cs, cn);
-    start_unit(cb, ckvh, cs);
-    int seg_g = run_a;
-    int buf = 0;
-
-    for (int gt = run_a; gt < run_e; ++gt, buf ^= 1) {
-      const int b = cb, kvh = ckvh, j = cj, n = cn;
-      const uint32_t s = cs;
-      wait_all();        // this tile's DMA (and the previous piece's stores) are done
-      __syncthreads();   // ... for every wave; every wave is done with the other buffer
-      // the owner's run grows by the next tail chunk if its claim was won
-      if (owner && gt == run_e - 1 && ext < issued) {
-        if (sh_int[1]) {
-          run_e += sc.cs;
-          ++ext;
-          claim_tile = ext < sc.nt ? max(gt + 1, sc.head_end(pid) + ext * sc.cs - 2) : -1;
-        } else {
-          claim_tile = -1;
+    for (int v = 0;; ++v) {
+      if (v >= count && pub0.state == 2 && pub1.state == 2) break;
+      const int st = v % kStages;
+      const bool due0 = pub0.state == 0 && v >= pub0.v + 2;
+      const bool due1 = pub1.state == 0 && v >= pub1.v + 2;
+      if constexpr (kProducer) {
+        if (v < count) wait_tile(min(kStages - 2, count - 1 - v));
+      } else {
+        if (due0 || due1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's piece stores
+        if (ctid == 0 && (pub0.state == 1 || pub1.state == 1)) {
+          const bool k0 = pub0.state == 1;
+          int uf, un;
+          unit_tiles(k0 ? pub0.unit : pub1.unit, uf, un);
+          const int np = sc.owner(uf + un - 1) - sc.owner(uf) + 1;   // pieces of the unit
+          sh_flag[v & 1] = (k0 ? pub0.old : pub1.old) + 1 == np ? 1 : 0;
         }
       }
-      const bool seg_first = gt == run_a || j == 0;
-      const bool seg_last = gt == run_e - 1 || j == n - 1;
-      const bool publishing = pub_pending;
-      const int is_last = publishing ? count_piece() : 0;
-      const bool claiming = owner && gt == claim_tile && issued < sc.nt;
-      if (claiming && tid == 0) claim_res = claim(pid, issued);
-      if (claiming) ++issued;
-      if (gt + 1 < run_e) {
-        if (++cj == cn) {
-          cj = 0;
-          if (++ckvh == Hkv) {
-            ckvh = 0;
-            do {
-              ++cb;
-            } while (seq_tiles<C>(seqs[cb]) == 0);   // in range: the next tile exists
-            cs = seqs[cb];
-            cn = seq_tiles<C>(cs);
+      lds_barrier();   // tile v is in LDS; every wave is done with tile v - 1 and its merges
+      if constexpr (kProducer) {
+        if (dv < count) {
+          dma(dcur, dv % kStages);
+          if (dv + 1 < count) advance(dcur, dv);
+          ++dv;
+        }
+      }
+      if (pub0.state == 1 || pub1.state == 1) {
+        // the last piece of a unit merges it
+        const bool k0 = pub0.state == 1;
+        const int unit = k0 ? pub0.unit : pub1.unit;
+        if (k0) pub0.state = 2;
+        else pub1.state = 2;
+        if constexpr (!kProducer) {
+          if (sh_flag[v & 1]) {
+            int uf, un;
+            unit_tiles(unit, uf, un);
+            merge_unit<D>(p, sc, seqs, ctid, unit, uf, un);
           }
         }
-        dma_tile(buf ^ 1, cb, ckvh, cj, cs, cn);
       }
+      if (due0 || due1) {
+        Pub& q = due0 ? pub0 : pub1;
+        if constexpr (!kProducer) {
+          if (ctid == 0)
+            q.old = __hip_atomic_fetch_add(p.counters + q.unit, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        q.state = 1;
+      }
+      if (v >= count) continue;
 
-      const char* ks = smem + buf * 2 * C::kLdsTile;
-      const char* vs = ks + C::kLdsTile;
-      const int T = seq_T(s);
-      const int hi = T - (n - 1 - j) * C::kTileKeys;
-      const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
-      const int nk = hi - lo;
-
+      const int b = cur.b, kvh = cur.kvh, j = cur.j;
+      const uint32_t s = cur.s;
+      const int n = seq_tiles<C>(s);
+      const int gt = tile_at(v);
+      const bool seg_first = v == 0 || v == nL || j == 0;
+      const bool seg_last = v == count - 1 || v + 1 == nL || j == n - 1;
       if (seg_first) {
-        seg_g = gt;
+        roles(cur);
+        if constexpr (!kProducer) {
+          // qr holds this unit's Q; the next segment's Q arrives meanwhile
+          int v_next;
+          const Cursor nx = next_segment(cur, v, v_next);
+          if (v_next < count) load_q(nx, qn);
 #pragma unroll
-        for (int dc = 0; dc < C::kDC; ++dc) o[dc] = f32x16{};
-        m_run = -INFINITY;   // running row max, log2 units
-        l_run = 0.f;         // running row sum of 2^(s - m_run)
+          for (int db = 0; db < C::kDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+          m_run = -INFINITY;
+          l_lane = 0.f;
+        }
+        seg_g = gt;
       }
 
-      if (has_rows) {
-        const int dc_lo = dh * (C::kDC / n_dh);
-        const int dc_hi = dc_lo + C::kDC / n_dh;
-        for (int sub = kg; sub < C::kNSub; sub += n_kg) {
-          if (sub * kSub >= nk) break;
-          const int key0 = lo + sub * kSub;            // absolute index of the subtile's key 0
-          const int krow = sub * kSub + lr;            // this lane's K row in the tile
-
-          // S^T = K Q^T for 32 keys x 32 rows
-          f32x16 sacc = f32x16{};
-#pragma unroll
-          for (int j2 = 0; j2 < C::kQChunks; ++j2) {
-            const u32x4 kop = *reinterpret_cast<const u32x4*>(ks + lds_off<C>(krow, 2 * j2 + half));
+      if constexpr (!kProducer) {
+        if (active) {
+          const char* ks = smem + st * C::kStage;
+          const char* vs = ks + C::kLdsHalf;
+          const int T = seq_T(s);
+          const int hi = T - (n - 1 - j) * C::kTileKeys;
+          const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
+          const int nk = hi - lo;
+          for (int kb = kslot; kb < C::kNKB; kb += kw) {
+            if (kb * kBlk >= nk) break;
+            const int key0 = lo + kb * kBlk;
+            // V^T operands first (they do not depend on the scores): lane
+            // (lm, lg) needs V rows key0 + 4 lg + e, e = 0..3, at d = 16 db + lm.
+            // bf16: one transposed LDS read per d block, in which lane t of the
+            // 16-lane group lg points at row key0 + 4 lg + t / 4, columns
+            // 16 db + 4 (t % 4) .. + 3.
+            i16x4 vt[BF16 ? C::kDB : 1];
+            float vf[BF16 ? 1 : C::kDB * 4];
             if constexpr (BF16) {
-              sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, kop),
-                                                             __builtin_bit_cast(bf16x8, qreg[j2]), sacc, 0, 0, 0);
+              typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+              const char* vrow = vs + (kb * kBlk + 4 * lg + (lm >> 2)) * C::kPitch + 8 * (lm & 3);
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db)
+                vt[db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + 32 * db));
+            } else {
+              const char* vrow = vs + (kb * kBlk + 4 * lg) * C::kPitch + 4 * lm;
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                  vf[4 * db + r] = *reinterpret_cast<const float*>(vrow + r * C::kPitch + 64 * db);
+            }
+
+            // S^T = K Q^T for 16 keys x 16 rows; lane (row lm, quarter lg)
+            // gets the keys key0 + 4 lg + r, r = 0..3
+            const char* krow = ks + (kb * kBlk + lm) * C::kPitch + 16 * lg;
+            u32x4 kop[C::kQJ];
+#pragma unroll
+            for (int J = 0; J < C::kQJ; ++J) kop[J] = *reinterpret_cast<const u32x4*>(krow + 64 * J);
+            f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int J = 0; J < C::kQJ; ++J) {
+              if constexpr (BF16) {
+                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[J]),
+                                                             __builtin_bit_cast(bf16x8, qr[J]), sa, 0, 0, 0);
+              } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                  sa = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kop[J][e]), __uint_as_float(qr[J][e]),
+                                                            sa, 0, 0, 0);
+              }
+            }
+
+            // scale, mask, online softmax
+            const bool edge = (key0 + kBlk > hi) || (key0 + kBlk - 1 > l_ctx);
+            float x[4];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              x[r] = sa[r] * p.sl2;
+              if (edge) {
+                const int key = key0 + 4 * lg + r;
+                if (key >= hi || key > vis) x[r] = -INFINITY;
+              }
+              mx = fmaxf(mx, x[r]);
+            }
+            mx = row_max(mx);
+            // raise the running max only when the block's max passes it by
+            // more than kLazyMax; the four lanes of a row decide alike
+            const bool raise = mx > m_run + kLazyMax;
+            if (__any(raise)) {
+              const float m_new = raise ? mx : m_run;
+              const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
+              l_lane *= alpha;
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db) o[db] *= alpha;
+              m_run = m_new;
+            }
+            const float m_use = m_run == -INFINITY ? 0.f : m_run;
+            float pr[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              pr[r] = __builtin_amdgcn_exp2f(x[r] - m_use);
+              l_lane += pr[r];
+            }
+
+            // O^T += V^T P^T
+            if constexpr (BF16) {
+              i16x4 pb;
+              {
+                const uint32_t p01 = pack_bf16x2(pr[0], pr[1]);
+                const uint32_t p23 = pack_bf16x2(pr[2], pr[3]);
+                pb[0] = (short)(p01 & 0xffffu);
+                pb[1] = (short)(p01 >> 16);
+                pb[2] = (short)(p23 & 0xffffu);
+                pb[3] = (short)(p23 >> 16);
+              }
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db)
+                o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt[db], pb, o[db], 0, 0, 0);
             } else {
 #pragma unroll
-              for (int e = 0; e < 4; ++e)
-                sacc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(kop[e]),
-                                                            __uint_as_float(qreg[j2][e]), sacc, 0, 0, 0);
-            }
-          }
-
-          // scale, mask, online softmax; lane holds row `row`, keys
-          // key0 + 8*(r/4) + 4*half + r%4 for r = 0..15
-          const bool edge = (key0 + kSub > hi) || (key0 + kSub - 1 > l_ctx);
-          float mx = -INFINITY;
+              for (int db = 0; db < C::kDB; ++db)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            float x = sacc[r] * p.sl2;
-            if (edge) {
-              const int key = key0 + 8 * (r >> 2) + 4 * half + (r & 3);
-              if (key >= hi || key > vis) x = -INFINITY;
-            }
-            sacc[r] = x;
-            mx = fmaxf(mx, x);
-          }
-          mx = fmaxf(mx, xor32(mx));
-          const float m_new = fmaxf(m_run, mx);
-          const float m_use = m_new == -INFINITY ? 0.f : m_new;
-          const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-          float rs = 0.f;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            sacc[r] = __builtin_amdgcn_exp2f(sacc[r] - m_use);
-            rs += sacc[r];
-          }
-          rs += xor32(rs);
-          l_run = l_run * alpha + rs;
-          m_run = m_new;
-#pragma unroll
-          for (int dc = 0; dc < C::kDC; ++dc)
-            if (dc >= dc_lo && dc < dc_hi) o[dc] *= alpha;
-
-          // O^T += V^T P^T for this wave's d blocks
-          if constexpr (BF16) {
-            u32x4 pb[2];
-#pragma unroll
-            for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-              for (int w = 0; w < 4; ++w)
-                pb[t2][w] = pack_bf16x2(sacc[8 * t2 + 2 * w], sacc[8 * t2 + 2 * w + 1]);
-#pragma unroll
-            for (int dc = 0; dc < C::kDC; ++dc) {
-              if (dc < dc_lo || dc >= dc_hi) continue;
-              const int d = dc * 32 + lr;
-#pragma unroll
-              for (int t2 = 0; t2 < 2; ++t2) {
-                // A operand: V[key(e)][d] for the 8 keys e of this lane's k half
-                i16x8 vop;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const int vrow = sub * kSub + 16 * t2 + 8 * (e >> 2) + 4 * half + (e & 3);
-                  vop[e] = *reinterpret_cast<const short*>(vs + lds_off<C>(vrow, d >> 3) + 2 * (d & 7));
-                }
-                o[dc] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, vop),
-                                                                __builtin_bit_cast(bf16x8, pb[t2]), o[dc], 0, 0, 0);
-              }
-              // keep the gathers of one 32-wide d block live at a time
-              __builtin_amdgcn_sched_barrier(0);
-            }
-          } else {
-#pragma unroll
-            for (int dc = 0; dc < C::kDC; ++dc) {
-              if (dc < dc_lo || dc >= dc_hi) continue;
-              const int d = dc * 32 + lr;
-#pragma unroll
-              for (int u = 0; u < 16; ++u) {
-                const int vrow = sub * kSub + 8 * (u >> 2) + 4 * half + (u & 3);
-                const float x = *reinterpret_cast<const float*>(vs + lds_off<C>(vrow, d >> 2) + 4 * (d & 3));
-                o[dc] = __builtin_amdgcn_mfma_f32_32x32x2f32(x, sacc[u], o[dc], 0, 0, 0);
-              }
+                for (int r = 0; r < 4; ++r)
+                  o[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf[4 * db + r], pr[r], o[db], 0, 0, 0);
             }
           }
         }
       }
 
-      // scratch space for merges: this tile's buffer, which every wave is
-      // done reading after the merges' first barrier (the next DMA goes to
-      // the other buffer)
-      char* scratch = smem + buf * 2 * C::kLdsTile;
-
-      // the counted piece: the one that completes its unit merges it
-      if (publishing) {
-        if (tid == 0) sh_int[2] = is_last;
-        __syncthreads();
-        if (sh_int[2]) merge_unit<D>(p, sc, seqs, scratch, mark, pub_unit, pub_first, pub_n);
-        pub_pending = false;
-      }
-      // the owner's claim result, for the next tile's run extension
-      if (claiming && tid == 0) sh_int[1] = claim_res;
-      if (!seg_last) continue;
-
-      // ---- end of a segment: merge the key groups of each (row tile, d
-      // half) through LDS
-      const int dc_lo = dh * (C::kDC / n_dh);
-      const int dc_hi = dc_lo + C::kDC / n_dh;
-      if (n_kg > 1) {
-        __syncthreads();
-        float* mbuf = reinterpret_cast<float*>(scratch);
-        constexpr int kRegion = 128 + C::kDC * 16 * 64;   // stats (2 x 64) then O
-        const int region = ((kg - 1) * n_rt4 + rt) * n_dh + dh;
-        if (kg > 0 && has_rows) {
-          float* reg = mbuf + region * kRegion;
-          reg[lane] = m_run;
-          reg[64 + lane] = l_run;
+      if (seg_last) {
+        // the next segment's Q (loaded a segment ago) becomes current before
+        // this segment's results are stored, so its wait covers no store
+        if constexpr (!kProducer) {
 #pragma unroll
-          for (int dc = 0; dc < C::kDC; ++dc)
-            if (dc >= dc_lo && dc < dc_hi)
-#pragma unroll
-              for (int r = 0; r < 16; ++r) reg[128 + ((dc - dc_lo) * 16 + r) * 64 + lane] = o[dc][r];
+          for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
         }
-        __syncthreads();
-        if (kg == 0 && has_rows) {
-          float M = m_run;
-          for (int k2 = 1; k2 < n_kg; ++k2)
-            M = fmaxf(M, mbuf[(((k2 - 1) * n_rt4 + rt) * n_dh + dh) * kRegion + lane]);
-          const float Muse = M == -INFINITY ? 0.f : M;
-          const float a0 = __builtin_amdgcn_exp2f(m_run - Muse);
-          l_run *= a0;
+        // ---- merge the key-split states of each row block through LDS
+        // (pairwise tree; this tile's stage is the scratch, and the next load
+        // into it is issued only after the next iteration's barrier)
+        char* scratch = smem + st * C::kStage;
+        for (int step = 1; step < nks; step <<= 1) {
+          lds_barrier();
+          if constexpr (!kProducer) {
+            const int region = rb + n_rbp * (kslot / (2 * step));
+            f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
+            if (active && (kslot & (2 * step - 1)) == step) {
 #pragma unroll
-          for (int dc = 0; dc < C::kDC; ++dc) o[dc] *= a0;
-          for (int k2 = 1; k2 < n_kg; ++k2) {
-            const float* reg = mbuf + (((k2 - 1) * n_rt4 + rt) * n_dh + dh) * kRegion;
-            const float w = __builtin_amdgcn_exp2f(reg[lane] - Muse);
-            l_run += reg[64 + lane] * w;
-#pragma unroll
-            for (int dc = 0; dc < C::kDC; ++dc)
-              if (dc >= dc_lo && dc < dc_hi)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) o[dc][r] += w * reg[128 + ((dc - dc_lo) * 16 + r) * 64 + lane];
+              for (int db = 0; db < C::kDB; ++db) reg[db * 64 + lane] = o[db];
+              mst[region][0][lane] = m_run;
+              mst[region][1][lane] = l_lane;
+            }
           }
-          m_run = M;
+          lds_barrier();
+          if constexpr (!kProducer) {
+            const int region = rb + n_rbp * (kslot / (2 * step));
+            const f32x4* reg = reinterpret_cast<const f32x4*>(scratch + region * (64 * D));
+            if (active && (kslot & (2 * step - 1)) == 0 && kslot + step < nks) {
+              const float mo = mst[region][0][lane];
+              const float lo2 = mst[region][1][lane];
+              const float M = fmaxf(m_run, mo);
+              const float Mu = M == -INFINITY ? 0.f : M;
+              const float wa = __builtin_amdgcn_exp2f(m_run - Mu);
+              const float wb = __builtin_amdgcn_exp2f(mo - Mu);
+              l_lane = l_lane * wa + lo2 * wb;
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db) o[db] = o[db] * wa + reg[db * 64 + lane] * wb;
+              m_run = M;
+            }
+          }
         }
-      }
 
-      // ---- write: the whole unit (final result) or a piece of it.  Every
-      // valid row saw at least one key of the segment, so l_run > 0.
-      const int unit_first = gt - j;                 // global index of the unit's tile 0
-      const bool whole = seg_g == unit_first && j == n - 1;
-      const bool first_of_run = seg_g == run_a;
-      const int slot = 2 * sc.sub_index(first_of_run ? run_a : seg_g) + (first_of_run ? 0 : 1);
-      const int unit = b * Hkv + kvh;
-      if (kg == 0 && row_valid) {
-        const float inv = 1.f / l_run;
-        const float lse_val = (m_run + log2f(l_run)) * kLn2;
-        if (whole) {
-          const size_t orow = (size_t)(b * p.C_max + tok) * p.Hq + kvh * g + row % g;
-          float* dst = p.out + orow * D;
-          if (half == 0 && dh == 0) p.lse[orow] = lse_val;
+        // ---- write: the whole unit (final result) or a piece of it
+        const int unit_first = gt - j;                 // global index of the unit's tile 0
+        const bool whole = seg_g == unit_first && j == n - 1;
+        if constexpr (!kProducer) {
+          const int slot = 2 * pid + (seg_g == g0 ? 0 : 1);
+          if (active && kslot == 0) {
+            const float l_row = row_sum(l_lane);
+            if (row_valid) {
+              const float inv = l_row > 0.f ? 1.f / l_row : 0.f;
+              const float lse_val = l_row > 0.f ? (m_run + log2f(l_row)) * kLn2 : -INFINITY;
+              if (whole) {
+                const size_t orow = (size_t)(b * p.C_max + tok) * p.Hq + kvh * g + row % g;
+                float* dst = p.out + orow * D;
+                if (lg == 0) p.lse[orow] = lse_val;
 #pragma unroll
-          for (int dc = 0; dc < C::kDC; ++dc)
-            if (dc >= dc_lo && dc < dc_hi)
+                for (int db = 0; db < C::kDB; ++db)
+                  *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = o[db] * inv;
+              } else {
+                // read by another workgroup, possibly on another XCD
+                const __amdgpu_buffer_rsrc_t ws_o_rsrc =
+                    __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
+                const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
+                    __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
+                const int srow = slot * p.Rcap + row;
+                if (lg == 0)
+                  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, lse_val), ws_lse_rsrc, srow * 4, 0,
+                                                        kDeviceCoherent);
 #pragma unroll
-              for (int g4 = 0; g4 < 4; ++g4) {
-                const int d0 = dc * 32 + 8 * g4 + 4 * half;
-                *reinterpret_cast<f32x4*>(dst + d0) = f32x4{o[dc][4 * g4] * inv, o[dc][4 * g4 + 1] * inv,
-                                                            o[dc][4 * g4 + 2] * inv, o[dc][4 * g4 + 3] * inv};
+                for (int db = 0; db < C::kDB; ++db)
+                  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, o[db] * inv), ws_o_rsrc,
+                                                         (srow * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent);
               }
-        } else {
-          // read by another workgroup, possibly on another XCD: device-coherent stores
-          const int srow = slot * p.Rcap + row;
-          if (half == 0 && dh == 0)
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, lse_val), ws_lse_rsrc, srow * 4, 0,
-                                                  kDeviceCoherent);
-#pragma unroll
-          for (int dc = 0; dc < C::kDC; ++dc)
-            if (dc >= dc_lo && dc < dc_hi)
-#pragma unroll
-              for (int g4 = 0; g4 < 4; ++g4) {
-                const int d0 = dc * 32 + 8 * g4 + 4 * half;
-                const f32x4 val = {o[dc][4 * g4] * inv, o[dc][4 * g4 + 1] * inv, o[dc][4 * g4 + 2] * inv,
-                                   o[dc][4 * g4 + 3] * inv};
-                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, val), ws_o_rsrc,
-                                                       (srow * D + d0) * 4, 0, kDeviceCoherent);
-              }
+            }
+          }
+        }
+        if (!whole) {
+          Pub q;
+          q.state = 0;
+          q.unit = b * Hkv + kvh;
+          q.v = v;
+          q.old = 0;
+          if (n_pub == 0) pub0 = q;
+          else pub1 = q;
+          ++n_pub;
         }
       }
-      if (!whole) {
-        if (tid == 0) {
-          __builtin_amdgcn_raw_buffer_store_b32(mark, ws_tag_rsrc, slot * 8, 0, kDeviceCoherent);
-          __builtin_amdgcn_raw_buffer_store_b32(unit, ws_tag_rsrc, slot * 8 + 4, 0, kDeviceCoherent);
-        }
-        pub_pending = true;
-        pub_unit = unit;
-        pub_first = unit_first;
-        pub_n = n;
-        pub_tiles = gt - seg_g + 1;
-      }
-      // the next tile starts a new unit: load its Q now, so that it arrives
-      // while this workgroup waits for the next tile anyway
-      if (gt + 1 < run_e) start_unit(cb, ckvh, cs);
+      if (v + 1 < count) advance(cur, v);
     }
-
-    // ---- the run's last piece is still to be counted
-    if (pub_pending) {
-      wait_all();
-      __syncthreads();
-      const int is_last = count_piece();
-      if (tid == 0) sh_int[2] = is_last;
-      __syncthreads();
-      if (sh_int[2]) merge_unit<D>(p, sc, seqs, smem, mark, pub_unit, pub_first, pub_n);
-      pub_pending = false;
-    }
-
-    // ---- steal: probe tail chunks, the last chunk of every range first.
-    // Every workgroup ends on one exhausted probe, also without stealing
-    // (nt = 0): the launch's last probe advances the generation, so that no
-    // call can mistake a piece tag of an earlier call for one of its own.
-    owner = false;
-    const int total_probes = sc.Pe * (sc.nt + 1);
-    int got = -1;
-    for (;;) {
-      if (tid == 0) {
-        const int k = __hip_atomic_fetch_add(p.thief_ctr, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        int res = -2;                                  // chunk taken: probe again
-        if (k >= sc.Pe * sc.nt) {
-          res = -1;                                    // nothing left
-          if (k == total_probes - 1) {                 // the launch's last probe: next call's state
-            __hip_atomic_store(p.thief_ctr, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(p.gen, mark, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          }
-        } else {
-          const int q = k % sc.Pe;
-          const int i = sc.nt - 1 - k / sc.Pe;
-          if (claim(q, i)) res = k;
-        }
-        sh_int[3] = res;
-      }
-      __syncthreads();
-      const int res = sh_int[3];
-      __syncthreads();
-      if (res != -2) {
-        got = res;
-        break;
-      }
-    }
-    if (got < 0) break;
-    const int q = got % sc.Pe;
-    const int i = sc.nt - 1 - got / sc.Pe;
-    run_a = sc.sub_begin(q, 1 + i);
-    run_e = run_a + sc.cs;
-  }
+  };
+  if (producer) run(std::true_type{});
+  else run(std::false_type{});
 }
 
-// Zero the state region and the piece tags of a workspace.
-__global__ void zero_state_kernel(int* state, int n_state, int* tags, int n_tags) {
+// Zero the per-unit counters of a workspace.
+__global__ void zero_counters_kernel(int* counters, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n_state) state[i] = 0;
-  else if (i - n_state < n_tags) tags[i - n_state] = 0;
+  if (i < n) counters[i] = 0;
 }
 
 // ---------------------------------------------------------------- host side
 
 int key_tile(int dtype, int D) {
   const int elt = dtype == SPECMOE_BF16 ? 2 : 4;
-  return kTileBytes / (D * elt);
+  return kHalf / (D * elt);
 }
 
-// Workspace layout.  The state region has the same layout for every
-// descriptor with the same Hkv: generation and probe counter at offset 0,
-// claim marks for the largest grid, per-unit counters for the largest launch.
-// Only the piece region (tags, lse, O) depends on the grid and the shape, and
-// a piece is only read under a tag of the current call's generation.
+// Workspace layout: per-unit arrival counters for the largest launch (same
+// offsets for every descriptor with the same Hkv), then the partial results
+// of the pieces, two slots per workgroup.
 struct Plan {
   int g, P, Rcap;
-  size_t claims_off, counters_off, counter_bytes;   // state region: [0, counter_bytes)
-  size_t slots, ws_tag_off, ws_lse_off, ws_o_off, ws_bytes;
+  size_t counter_bytes;
+  size_t slots, ws_lse_off, ws_o_off, ws_bytes;
 };
-
-constexpr int kMaxGrid = 2048;         // merge candidates (10 per range) are flagged in one 34 KB tile buffer
 
 int validate_desc(const specmoe_verify_desc* d) {
   if (!d) return SPECMOE_ERR_NULL_POINTER;
@@ -827,12 +838,11 @@ int validate_desc(const specmoe_verify_desc* d) {
   if (d->Hq % d->Hkv != 0) return SPECMOE_ERR_GQA;
   const int64_t g = d->Hq / d->Hkv;
   if ((int64_t)d->C_max * g > kMaxRows) return SPECMOE_ERR_ROWS;
-  if (d->flags & ~SPECMOE_DETERMINISTIC) return SPECMOE_ERR_FLAGS;
+  if (d->flags != 0) return SPECMOE_ERR_FLAGS;
   if (d->grid_blocks < 0 || d->grid_blocks > kMaxGrid) return SPECMOE_ERR_GRID;
-  // partial results are addressed through 32-bit buffer descriptors: up to
-  // 10 pieces per workgroup (2 per sub-range, 5 sub-ranges per range)
+  // partial results are addressed through 32-bit buffer descriptors
   const int64_t grid = d->grid_blocks ? d->grid_blocks : kDefaultGrid;
-  if (10 * grid * (int64_t)d->C_max * g * d->D * 4 >= ((int64_t)1 << 31)) return SPECMOE_ERR_GRID;
+  if (2 * grid * (int64_t)d->C_max * g * d->D * 4 >= ((int64_t)1 << 31)) return SPECMOE_ERR_GRID;
   // index arithmetic: (sequence, token, head) row indices stay in 32 bits,
   // byte offsets inside one (sequence, KV head) slab are 32-bit, packed
   // sequence lengths need T < 2^24, tile counts per launch stay in 32 bits.
@@ -852,12 +862,9 @@ Plan make_plan(const specmoe_verify_desc* d) {
   pl.g = d->Hq / d->Hkv;
   pl.P = d->grid_blocks ? d->grid_blocks : kDefaultGrid;
   pl.Rcap = d->C_max * pl.g;
-  pl.claims_off = 256;
-  pl.counters_off = pl.claims_off + (size_t)kMaxGrid * 4 * sizeof(int);
-  pl.counter_bytes = align256(pl.counters_off + (size_t)kMaxSeqs * d->Hkv * sizeof(int));
-  pl.slots = (size_t)10 * pl.P;
-  pl.ws_tag_off = pl.counter_bytes;
-  pl.ws_lse_off = pl.ws_tag_off + align256(pl.slots * 2 * sizeof(int));
+  pl.counter_bytes = align256((size_t)kMaxSeqs * d->Hkv * sizeof(int));
+  pl.slots = (size_t)2 * pl.P;
+  pl.ws_lse_off = pl.counter_bytes;
   pl.ws_o_off = pl.ws_lse_off + align256(pl.slots * pl.Rcap * sizeof(float));
   pl.ws_bytes = pl.ws_o_off + pl.slots * pl.Rcap * d->D * sizeof(float);
   return pl;
@@ -904,13 +911,10 @@ int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, 
   if (!aligned16(workspace)) return SPECMOE_ERR_ALIGN;
   const Plan pl = make_plan(desc);
   if (workspace_bytes < pl.ws_bytes) return SPECMOE_ERR_WORKSPACE;
-  const int n_state = (int)(pl.counter_bytes / sizeof(int));
-  const int n_tags = (int)((pl.ws_lse_off - pl.ws_tag_off) / sizeof(int));
-  char* ws = static_cast<char*>(workspace);
+  const int n = (int)(pl.counter_bytes / sizeof(int));
   (void)hipGetLastError();
-  hipLaunchKernelGGL(zero_state_kernel, dim3((n_state + n_tags + 255) / 256), dim3(256), 0,
-                     static_cast<hipStream_t>(stream), reinterpret_cast<int*>(ws), n_state,
-                     reinterpret_cast<int*>(ws + pl.ws_tag_off), n_tags);
+  hipLaunchKernelGGL(zero_counters_kernel, dim3((n + 255) / 256), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<int*>(workspace), n);
   return hipGetLastError() == hipSuccess ? SPECMOE_OK : SPECMOE_ERR_LAUNCH;
 }
 
@@ -931,7 +935,7 @@ const char* specmoe_status_str(int status) {
     case SPECMOE_ERR_DTYPE: return "unsupported dtype";
     case SPECMOE_ERR_ROWS: return "C_max * (Hq / Hkv) exceeds 128 query rows per KV head";
     case SPECMOE_ERR_GRID: return "grid_blocks must be 0 (default) or in [1, 2048], with partial results under 2 GB";
-    case SPECMOE_ERR_FLAGS: return "unknown bits in flags";
+    case SPECMOE_ERR_FLAGS: return "flags is reserved and must be 0";
     case SPECMOE_ERR_WORKSPACE: return "workspace too small";
     case SPECMOE_ERR_ALIGN: return "q, k_cache, v_cache, out and workspace must be 16-byte aligned";
     case SPECMOE_ERR_SCALE: return "scale is not finite";
@@ -963,17 +967,11 @@ int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
   p.out = out;
   p.lse = lse;
   char* ws = static_cast<char*>(desc->workspace);
-  p.gen = reinterpret_cast<int*>(ws);
-  p.thief_ctr = p.gen + 1;
-  p.claims = reinterpret_cast<int*>(ws + pl.claims_off);
-  p.counters = reinterpret_cast<int*>(ws + pl.counters_off);
-  p.ws_tag = reinterpret_cast<int*>(ws + pl.ws_tag_off);
+  p.counters = reinterpret_cast<int*>(ws);
   p.ws_lse = reinterpret_cast<float*>(ws + pl.ws_lse_off);
   p.ws_o = reinterpret_cast<float*>(ws + pl.ws_o_off);
-  p.ws_tag_bytes = (int)(pl.ws_lse_off - pl.ws_tag_off);
   p.ws_lse_bytes = (int)(pl.ws_o_off - pl.ws_lse_off);
   p.ws_o_bytes = (int)(pl.ws_bytes - pl.ws_o_off);
-  p.deterministic = (desc->flags & SPECMOE_DETERMINISTIC) ? 1 : 0;
   p.B = desc->B;
   p.Hq = desc->Hq;
   p.Hkv = desc->Hkv;

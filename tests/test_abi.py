@@ -67,6 +67,7 @@ def _call(lib, desc, q=FAKE, k=FAKE, v=FAKE, ctx=FAKE, chunk=FAKE, scale=0.088, 
     (dict(C_max=17, Hq=32, Hkv=4), -6),          # 17 * 8 = 136 rows > 128
     (dict(grid_blocks=-1), -7),
     (dict(grid_blocks=2049), -7),
+    (dict(flags=1), -12),
     (dict(flags=2), -12),
     (dict(S_max=1 << 23), -2),                   # slab offsets would pass 2^31 bytes
     (dict(S_max=1 << 24, dtype=bd.SPECMOE_BF16, D=64), -2),   # packed lengths need T < 2^24
@@ -89,18 +90,17 @@ def test_null_and_alignment_and_scale(lib):
 
 
 def test_workspace_contract(lib):
-    d = _desc(B=64, grid_blocks=512)
+    d = _desc(B=64, grid_blocks=256)
     need = lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d))
     rows = 5 * 4                                # C_max * g
-    slots = 10 * 512 * rows                     # up to ten pieces per workgroup
-    state = 256 + 2048 * 4 * 4 + 1024 * 8 * 4  # generation + probe counter, claim marks, unit counters
-    tags = 10 * 512 * 8
-    assert need >= state + tags + slots * (128 + 1) * 4
-    assert need < state + tags + slots * (128 + 1) * 4 + 1024
+    slots = 2 * 256 * rows                      # two pieces per workgroup
+    counters = 1024 * 8 * 4                     # one per (sequence, KV head) of a launch
+    assert need >= counters + slots * (128 + 1) * 4
+    assert need < counters + slots * (128 + 1) * 4 + 512
     # the workspace grows with the grid
     d2 = _desc(B=64, grid_blocks=1024)
     assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d2)) > need
-    # default grid = 512 workgroups
+    # default grid = 256 workgroups
     assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(_desc(B=64))) == need
     assert _call(lib, d) == -1                  # workspace needed but NULL
     d.workspace, d.workspace_bytes = FAKE, need - 1
