@@ -45,7 +45,7 @@ def source_digest() -> str:
 def load_traffic(workload: str):
     """HBM bytes per launch of the main kernel from the committed rocprofv3
     counter summary, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"{MAIN_KERNEL}_{workload}_traffic.json")
+    path = os.path.join(ROOT, "profiles", f"{MAIN_KERNEL}_{workload}_traffic.txt")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -57,7 +57,8 @@ def load_traffic(workload: str):
 
 def cpu_baseline(inp, w, budget_s: float):
     """The fp64 oracle, timed on the host cores over a bounded sample of the
-    same workload: whole sequences, in order, until ~budget_s of work."""
+    same workload: whole sequences, in order (wrapping around the batch),
+    until ~budget_s of work."""
     from oracle import verify_attn_ref
     from paper_2508_21706_amd import workloads as wl
     try:
@@ -67,15 +68,14 @@ def cpu_baseline(inp, w, budget_s: float):
         blas_threads = 1
     done = []
     t_total = 0.0
-    for b in range(w.B):
+    while t_total < budget_s:
+        b = len(done) % w.B
         units = [(b, h) for h in range(w.Hkv)]
         t0 = time.perf_counter()
         verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], inp["ctx_lens"], inp["chunk_lens"],
                         w.scale, w.dtype, units=units)
         t_total += time.perf_counter() - t0
         done.append(b)
-        if t_total >= budget_s:
-            break
     ctx = inp["ctx_lens"][done]
     chunk = inp["chunk_lens"][done]
     kv = wl.algorithmic_kv_bytes(w, ctx, chunk)
@@ -84,8 +84,8 @@ def cpu_baseline(inp, w, budget_s: float):
         "unit": "GB/s",
         "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": f"{len(done)} of {w.B} sequences (all KV heads) of {w.name}, fp64 numpy oracle, "
-                  f"{t_total:.1f} s; {int(chunk.sum())} draft tokens -> "
+        "sample": f"{len(done)} sequences (all KV heads; {len(done) / w.B:.1f} passes over the {w.B} of "
+                  f"{w.name}), fp64 numpy oracle, {t_total:.1f} s; {int(chunk.sum())} draft tokens -> "
                   f"{chunk.sum() / t_total:.1f} verified tokens/s",
         "host": {"os_cpu_count": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
                  "cpu": platform.processor() or platform.machine()},
@@ -100,7 +100,10 @@ def main():
     ap.add_argument("--workload", default="mixtral_b64")
     ap.add_argument("--grid-blocks", type=int, default=0, help="persistent workgroups (0: library default)")
     ap.add_argument("--rotate", type=int, default=0, help="input sets (0: enough for >= 1 GB)")
-    ap.add_argument("--cpu-budget", type=float, default=15.0, help="seconds of oracle work; 0 skips")
+    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work; 0 skips")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
+                    help="instead of the benchmark, run a plain elementwise copy of MB MiB (float32 read, "
+                         "float32 write) 5 times: the known byte counts calibrate the HBM traffic counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the verification-attention path has no "
@@ -109,6 +112,15 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_probe:
+        n = args.copy_probe * (1 << 20) // 4
+        x = torch.ones(n, dtype=torch.float32, device="cuda:0")
+        y = torch.empty_like(x)
+        for _ in range(5):
+            torch.neg(x, out=y)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 5}))
+        return
     import paper_2508_21706_amd as pkg
     from paper_2508_21706_amd import workloads as wl
 
@@ -215,7 +227,9 @@ def main():
         "kv_bytes_per_step": kv_bytes,
         "roofline": {"bound": "hbm", "kernel": MAIN_KERNEL, "achieved": round(achieved, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "algorithmic_bytes_per_launch": launch_bytes,
+                     "traffic": traffic, "traffic_unit": "HBM bytes per launch",
+                     "traffic_over_algorithmic": round(traffic / launch_bytes, 4) if traffic else None,
+                     "algorithmic_bytes_per_launch": launch_bytes,
                      "avg_launch_us": round(main_avg_ms * 1e3, 3)},
         "cpu_baseline": cpu,
     }
