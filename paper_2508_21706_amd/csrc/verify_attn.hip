@@ -55,9 +55,9 @@ constexpr int kConsumers = 8;                 // waves that compute
 constexpr int kWaves = kProducers + kConsumers;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCThreads = 64 * kConsumers;
-constexpr int kStages = 4;                    // LDS ring of staged tiles
-constexpr int kHalf = 16384;                  // K bytes (and V bytes) of one tile
-constexpr int kMaxDma = 5;                    // DMA instructions per producer wave and K (or V) tile, at most
+constexpr int kStages = 2;                    // LDS ring of staged tiles
+constexpr int kHalf = 32768;                  // K bytes (and V bytes) of one tile
+constexpr int kMaxDma = 9;                    // DMA instructions per producer wave and K (or V) tile, at most
 constexpr int kBlk = 16;                      // keys (and query rows) per MFMA block
 constexpr int kMaxRows = 128;                 // row blocks per unit <= 8
 constexpr int kDefaultGrid = 256;             // persistent workgroups: one per CU of an MI355X
@@ -115,9 +115,10 @@ struct Cfg {
   static constexpr int kNKB = kTileKeys / kBlk;             // 16-key blocks per tile
   static constexpr int kDB = D / 16;                        // 16-wide d blocks of O^T
   static constexpr int kQJ = kChunks / 4;                   // 16-byte Q chunks per lane
-  static_assert(kInst <= 4 * kMaxDma && kInst >= 16 && kInst <= 18, "producer wait counts assume 16..18 DMA instructions");
-  static_assert(kStages * kStage + 12 * 1024 <= 160 * 1024, "LDS budget");
-  static_assert(4 * 64 * D <= kStage, "key-split merge scratch fits in a stage");
+  static_assert(kInst <= kProducers * kMaxDma, "DMA instructions per producer wave");
+  static_assert(kStages * kStage + 12 * 1024 + 256 <= 160 * 1024, "LDS budget");
+  static_assert(kConsumers * 64 * D <= kStage, "key-split merge scratch fits in a stage");
+  static_assert(kNKB >= 2, "key blocks are processed in pairs");
 };
 
 // Workgroup barrier that waits only for this wave's LDS operations.  A
@@ -188,9 +189,10 @@ struct Cursor {
 };
 
 // Merge every piece of a unit; run by the consumer threads of the workgroup
-// whose piece arrived last.  Range q's piece of the unit is its first
-// segment (slot 2q), except when range q starts before the unit: then it is
-// q's last segment (slot 2q+1).
+// whose piece arrived last, after its own tiles.  Range q's piece of the unit
+// is its first segment (slot 2q), except when range q starts before the
+// unit: then it is q's last segment (slot 2q+1).  Each thread takes two
+// (row, 4 d) items per round and issues all their loads before it waits.
 template <int D>
 __device__ __forceinline__ void merge_unit(const Params& p, const Sched& sc, const uint32_t* seqs, int ctid,
                                         int unit, int unit_first, int n_unit) {
@@ -203,42 +205,64 @@ __device__ __forceinline__ void merge_unit(const Params& p, const Sched& sc, con
   const int ub = unit / p.Hkv;
   const int ukvh = unit - ub * p.Hkv;
   const int g = p.g;
-  const int uR = seq_c(uniform(seqs[ub])) * g;
-  constexpr int kBatch = 4;
-  for (int idx = ctid; idx < uR * (D / 4); idx += kCThreads) {
-    const int r = idx / (D / 4);
-    const int d0 = 4 * (idx - r * (D / 4));
-    float m = -INFINITY, z = 0.f;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int q0 = qf; q0 <= ql; q0 += kBatch) {
-      float lq[kBatch];
-      f32x4 x[kBatch];
+  const int n_items = seq_c(uniform(seqs[ub])) * g * (D / 4);
+  constexpr int kBatch = 4;   // pieces loaded per item before combining
+  constexpr int kItems = 2;   // items per thread and round
+  for (int base = ctid; base < n_items; base += kItems * kCThreads) {
+    float m[kItems], z[kItems];
+    f32x4 acc[kItems];
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int q = q0 + u;
-        const int srow = (q == qf ? slot_first : 2 * q) * p.Rcap + r;
-        if (q <= ql) {
-          lq[u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ws_lse_rsrc, srow * 4, 0,
-                                                                               kDeviceCoherent));
-          x[u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ws_o_rsrc, (srow * D + d0) * 4, 0,
-                                                                                kDeviceCoherent));
+    for (int it = 0; it < kItems; ++it) {
+      m[it] = -INFINITY;
+      z[it] = 0.f;
+      acc[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int q0 = qf; q0 <= ql; q0 += kBatch) {
+      float lq[kItems][kBatch];
+      f32x4 x[kItems][kBatch];
+#pragma unroll
+      for (int it = 0; it < kItems; ++it) {
+        const int idx = base + it * kCThreads;
+        const int r = idx / (D / 4);
+        const int d0 = 4 * (idx - r * (D / 4));
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          const int q = q0 + u;
+          const int srow = (q == qf ? slot_first : 2 * q) * p.Rcap + r;
+          if (idx < n_items && q <= ql) {
+            lq[it][u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ws_lse_rsrc, srow * 4, 0,
+                                                                                     kDeviceCoherent));
+            x[it][u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                     ws_o_rsrc, (srow * D + d0) * 4, 0, kDeviceCoherent));
+          }
         }
       }
 #pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        if (q0 + u > ql) break;
-        if (lq[u] == -INFINITY) continue;   // a piece in which this row sees no key
-        const float nm = fmaxf(m, lq[u]);
-        const float a = expf(m - nm);
-        const float w = expf(lq[u] - nm);
-        z = z * a + w;
-        acc = acc * a + w * x[u];
-        m = nm;
+      for (int it = 0; it < kItems; ++it) {
+        if (base + it * kCThreads >= n_items) continue;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          if (q0 + u > ql) break;
+          if (lq[it][u] == -INFINITY) continue;   // a piece in which this row sees no key
+          const float nm = fmaxf(m[it], lq[it][u]);
+          const float a = expf(m[it] - nm);
+          const float w = expf(lq[it][u] - nm);
+          z[it] = z[it] * a + w;
+          acc[it] = acc[it] * a + w * x[it][u];
+          m[it] = nm;
+        }
       }
     }
-    const size_t orow = (size_t)(ub * p.C_max + r / g) * p.Hq + ukvh * g + r % g;
-    *reinterpret_cast<f32x4*>(p.out + orow * D + d0) = acc * (1.f / z);
-    if (d0 == 0) p.lse[orow] = m + logf(z);
+#pragma unroll
+    for (int it = 0; it < kItems; ++it) {
+      const int idx = base + it * kCThreads;
+      if (idx >= n_items) continue;
+      const int r = idx / (D / 4);
+      const int d0 = 4 * (idx - r * (D / 4));
+      const size_t orow = (size_t)(ub * p.C_max + r / g) * p.Hq + ukvh * g + r % g;
+      *reinterpret_cast<f32x4*>(p.out + orow * D + d0) = acc[it] * (1.f / z[it]);
+      if (d0 == 0) p.lse[orow] = m[it] + logf(z[it]);
+    }
   }
   if (ctid == 0)   // ready for the next call
     __hip_atomic_store(p.counters + unit, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -250,9 +274,9 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
   __shared__ uint32_t seqs[kMaxSeqs];     // packed (T, c) of every sequence of the launch
   __shared__ int pref[kMaxSeqs + 1];      // tiles per KV head of the sequences before b
-  __shared__ float mst[4][2][64];         // key-split merge: running max and partial sums
+  __shared__ float mst[kConsumers][2][64];   // key-split merge: row max and row sum of each wave
   __shared__ int wave_sum[kWaves];
-  __shared__ int sh_flag[2];              // "the counted piece completed its unit", by iteration parity
+  __shared__ int sh_flag[2];              // "this piece completed its unit", for the two pieces
 
   const int pid = blockIdx.x;
   const int tid = threadIdx.x;
@@ -429,24 +453,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       }
     }
   };
-  // wait until this producer's loads of a tile have landed in LDS, with
-  // `later` tiles issued after it still in flight (loads complete in order)
-  const int per_tile = 2 * ((C::kInst - wave + kProducers - 1) / kProducers);   // 8 or 10
-  auto wait_tile = [&](int later) {
-    switch (later * per_tile) {
-      case 20: asm volatile("s_waitcnt vmcnt(20)" ::: "memory"); break;
-      case 16: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
-      case 10: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
-      case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-      default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    }
-  };
 
   // ---- consumer roles for the unit of cursor cu.  Rows are cut into
   // n_rb 16-row blocks (n_rbp = n_rb rounded up to a power of two); consumer
-  // wave wc takes row block rb = wc % n_rbp and the key blocks
-  // kslot, kslot + kw, ... of every tile, kw = 8 / n_rbp.
-  int R = 0, n_rbp = 1, kw = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
+  // wave wc takes row block rb = wc % n_rbp, and the nks waves of a row block
+  // share every tile's key blocks: wave kslot takes the pairs
+  // (kb, kb + nks) for kb = kslot, kslot + 2 nks, ...  (nks <= kNKB / 2, so
+  // every wave has whole pairs).
+  int R = 0, n_rbp = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
   bool active = false, row_valid = false;
   auto roles = [&](const Cursor& cu) {
     const int c = seq_c(cu.s);
@@ -454,10 +468,9 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     l_ctx = seq_T(cu.s) - c;
     const int n_rb = (R + kBlk - 1) / kBlk;
     n_rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : n_rb <= 4 ? 4 : 8;
-    kw = kConsumers / n_rbp;
-    nks = min(kw, C::kNKB);                   // consumers that share a row block
+    nks = min(kConsumers / n_rbp, C::kNKB / 2);   // consumers that share a row block
     rb = producer ? 0 : wc % n_rbp;
-    kslot = producer ? kw : wc / n_rbp;
+    kslot = producer ? nks : wc / n_rbp;
     active = !producer && rb < n_rb && kslot < nks;
     row = rb * kBlk + lm;
     row_valid = active && row < R;
@@ -474,7 +487,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int rb_ = wc % rbp;
     const int ks_ = wc / rbp;
     const int row_ = rb_ * kBlk + lm;
-    const bool ok = rb_ < n_rb && ks_ < min(kConsumers / rbp, C::kNKB) && row_ < uR;
+    const bool ok = rb_ < n_rb && ks_ < min(kConsumers / rbp, C::kNKB / 2) && row_ < uR;
     const int tk = ok ? row_ / g : 0;
     const char* qrow =
         p.q + ((size_t)(cu.b * p.C_max + tk) * p.Hq + cu.kvh * g + (ok ? row_ % g : 0)) * C::kRowBytes;
@@ -484,15 +497,15 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   };
 
   // Publication of pieces (at most two per workgroup: its first and last
-  // segment).  The consumers' piece stores are acknowledged two iterations
-  // later (their own wait, which no tile load shares), the piece is then
-  // counted, and the count is read back one iteration after that; at most one
-  // piece is counted per iteration.  The loop runs idle iterations after the
-  // last tile until every piece is done.
+  // segment).  A piece's stores are issued in the window after its segment;
+  // two iterations later the consumers wait for them (their own wait, which
+  // no tile load shares) and the piece is counted on its unit's arrival
+  // counter.  The counts are read back after the loop, where the last piece
+  // of a unit merges it.  The loop runs idle iterations after the last tile
+  // until every piece is counted.
   struct Pub {
-    int state;   // 0 stored, 1 counted, 2 done
+    int state;   // 0 stored, 1 counted, 2 no piece
     int unit, v;
-    int old;     // counter value before this piece (consumer thread 0)
   };
 
   // ---- the main loop, instantiated once for the producers and once for the
@@ -509,8 +522,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 #pragma unroll
     for (int J = 0; J < C::kQJ; ++J) qn[J] = u32x4{0u, 0u, 0u, 0u};
     float m_run = -INFINITY, l_lane = 0.f;
-    Pub pub0 = {2, 0, 0, 0}, pub1 = {2, 0, 0, 0};
+    Pub pub0 = {2, 0, 0}, pub1 = {2, 0, 0};
     int n_pub = 0;
+    // counter values before the two pieces (consumer thread 0), read after
+    // the loop, so the atomics' returns are never waited for inside it
+    int cnt0 = 0, cnt1 = 0;
 
     // start: the first tiles in flight, the first unit's Q
     Cursor dcur = first;                 // cursor of the next tile to load
@@ -526,56 +542,87 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       load_q(first, qn);
 #pragma unroll
       for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
+#pragma unroll
+      for (int J = 0; J < C::kQJ; ++J) asm volatile("" : "+v"(qr[J])::"memory");
+      int v1;
+      const Cursor c1 = next_segment(first, 0, v1);
+      if (v1 < count) load_q(c1, qn);   // the second segment's Q
     }
     Cursor cur = first;                  // cursor of the tile being computed
     int seg_g = g0;
+    // results of the segment that ended in the previous iteration, stored in
+    // this iteration's window: o[] (this wave's d blocks), and per lane the
+    // output (or workspace) row, 1 / row sum and the row's lse
+    bool pend = false, pend_whole = false, pend_ok = false;
+    int pend_row = 0;
+    float pend_inv = 0.f, pend_lse = 0.f;
 
     for (int v = 0;; ++v) {
-      if (v >= count && pub0.state == 2 && pub1.state == 2) break;
+      if (v >= count && pub0.state != 0 && pub1.state != 0 && !pend) break;
       const int st = v % kStages;
       const bool due0 = pub0.state == 0 && v >= pub0.v + 2;
       const bool due1 = pub1.state == 0 && v >= pub1.v + 2;
       if constexpr (kProducer) {
-        if (v < count) wait_tile(min(kStages - 2, count - 1 - v));
+        // this producer's loads of tile v have landed in LDS (with two
+        // stages it is the only tile in flight)
+        if (v < count) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       } else {
         if (due0 || due1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's piece stores
-        if (ctid == 0 && (pub0.state == 1 || pub1.state == 1)) {
-          const bool k0 = pub0.state == 1;
-          int uf, un;
-          unit_tiles(k0 ? pub0.unit : pub1.unit, uf, un);
-          const int np = sc.owner(uf + un - 1) - sc.owner(uf) + 1;   // pieces of the unit
-          sh_flag[v & 1] = (k0 ? pub0.old : pub1.old) + 1 == np ? 1 : 0;
-        }
       }
       lds_barrier();   // tile v is in LDS; every wave is done with tile v - 1 and its merges
+
+      // ---- window for the consumers' own global memory operations: the
+      // stores of the segment that ended in the previous iteration and the
+      // count of a stored piece.  The next tile's loads are issued only after
+      // it (a second barrier), so these operations do not queue behind a
+      // tile's worth of loads in the CU's memory pipeline.
+      const bool window = pend || due0 || due1;
+      if constexpr (!kProducer) {
+        if (pend && pend_ok) {
+          const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
+          const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
+          if (pend_whole) {
+            float* dst = p.out + (size_t)pend_row * D;
+            if (kslot == 0 && lg == 0) p.lse[pend_row] = pend_lse;
+#pragma unroll
+            for (int db = 0; db < C::kDB; ++db)
+              if (db >= d_lo && db < d_hi) *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = o[db] * pend_inv;
+          } else {
+            // read by another workgroup, possibly on another XCD
+            const __amdgpu_buffer_rsrc_t ws_o_rsrc =
+                __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
+            const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
+                __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
+            if (kslot == 0 && lg == 0)
+              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, pend_lse), ws_lse_rsrc, pend_row * 4, 0,
+                                                    kDeviceCoherent);
+#pragma unroll
+            for (int db = 0; db < C::kDB; ++db)
+              if (db >= d_lo && db < d_hi)
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, o[db] * pend_inv), ws_o_rsrc,
+                                                       (pend_row * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent);
+          }
+        }
+      }
+      pend = false;
+      if (due0 || due1) {
+        Pub& q = due0 ? pub0 : pub1;
+        if constexpr (!kProducer) {
+          if (ctid == 0) {
+            const int old = __hip_atomic_fetch_add(p.counters + q.unit, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (due0) cnt0 = old;
+            else cnt1 = old;
+          }
+        }
+        q.state = 1;
+      }
+      if (window) lds_barrier();
       if constexpr (kProducer) {
         if (dv < count) {
           dma(dcur, dv % kStages);
           if (dv + 1 < count) advance(dcur, dv);
           ++dv;
         }
-      }
-      if (pub0.state == 1 || pub1.state == 1) {
-        // the last piece of a unit merges it
-        const bool k0 = pub0.state == 1;
-        const int unit = k0 ? pub0.unit : pub1.unit;
-        if (k0) pub0.state = 2;
-        else pub1.state = 2;
-        if constexpr (!kProducer) {
-          if (sh_flag[v & 1]) {
-            int uf, un;
-            unit_tiles(unit, uf, un);
-            merge_unit<D>(p, sc, seqs, ctid, unit, uf, un);
-          }
-        }
-      }
-      if (due0 || due1) {
-        Pub& q = due0 ? pub0 : pub1;
-        if constexpr (!kProducer) {
-          if (ctid == 0)
-            q.old = __hip_atomic_fetch_add(p.counters + q.unit, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        q.state = 1;
       }
       if (v >= count) continue;
 
@@ -588,10 +635,6 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       if (seg_first) {
         roles(cur);
         if constexpr (!kProducer) {
-          // qr holds this unit's Q; the next segment's Q arrives meanwhile
-          int v_next;
-          const Cursor nx = next_segment(cur, v, v_next);
-          if (v_next < count) load_q(nx, qn);
 #pragma unroll
           for (int db = 0; db < C::kDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
           m_run = -INFINITY;
@@ -608,67 +651,78 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
           const int hi = T - (n - 1 - j) * C::kTileKeys;
           const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
           const int nk = hi - lo;
-          for (int kb = kslot; kb < C::kNKB; kb += kw) {
-            if (kb * kBlk >= nk) break;
-            const int key0 = lo + kb * kBlk;
+          // Key blocks kb0 and kb1 = kb0 + nks of the tile form a pair: two
+          // independent score chains, one softmax step over their 8 keys per
+          // lane, and (bf16) one 32-key P V contraction per d block.  A block
+          // past the tile's keys reads staged rows that hold finite data and
+          // is masked like any key >= hi.
+          for (int kb0 = kslot; kb0 < C::kNKB; kb0 += 2 * nks) {
+            if (kb0 * kBlk >= nk) break;
+            const int key0 = lo + kb0 * kBlk;
+            const int key1 = key0 + nks * kBlk;
+            const int bstride = nks * kBlk * C::kPitch;   // LDS bytes from block kb0 to kb1
             // V^T operands first (they do not depend on the scores): lane
-            // (lm, lg) needs V rows key0 + 4 lg + e, e = 0..3, at d = 16 db + lm.
-            // bf16: one transposed LDS read per d block, in which lane t of the
-            // 16-lane group lg points at row key0 + 4 lg + t / 4, columns
-            // 16 db + 4 (t % 4) .. + 3.
-            i16x4 vt[BF16 ? C::kDB : 1];
-            float vf[BF16 ? 1 : C::kDB * 4];
+            // (lm, lg) needs V rows key + 4 lg + e, e = 0..3, at d = 16 db + lm
+            // of both blocks.  bf16: one transposed LDS read per block and d
+            // block, in which lane t of the 16-lane group lg points at row
+            // key + 4 lg + t / 4, columns 16 db + 4 (t % 4) .. + 3.
+            i16x4 vt[BF16 ? 2 * C::kDB : 1];
             if constexpr (BF16) {
               typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-              const char* vrow = vs + (kb * kBlk + 4 * lg + (lm >> 2)) * C::kPitch + 8 * (lm & 3);
+              const char* vrow = vs + (kb0 * kBlk + 4 * lg + (lm >> 2)) * C::kPitch + 8 * (lm & 3);
 #pragma unroll
-              for (int db = 0; db < C::kDB; ++db)
-                vt[db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + 32 * db));
-            } else {
-              const char* vrow = vs + (kb * kBlk + 4 * lg) * C::kPitch + 4 * lm;
+              for (int h = 0; h < 2; ++h)
 #pragma unroll
-              for (int db = 0; db < C::kDB; ++db)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                  vf[4 * db + r] = *reinterpret_cast<const float*>(vrow + r * C::kPitch + 64 * db);
+                for (int db = 0; db < C::kDB; ++db)
+                  vt[h * C::kDB + db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                      (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + h * bstride + 32 * db));
             }
 
-            // S^T = K Q^T for 16 keys x 16 rows; lane (row lm, quarter lg)
-            // gets the keys key0 + 4 lg + r, r = 0..3
-            const char* krow = ks + (kb * kBlk + lm) * C::kPitch + 16 * lg;
-            u32x4 kop[C::kQJ];
+            // S^T = K Q^T for 16 keys x 16 rows per block; lane (row lm,
+            // quarter lg) gets the keys key + 4 lg + r, r = 0..3
+            const char* krow = ks + (kb0 * kBlk + lm) * C::kPitch + 16 * lg;
+            f32x4 sa[2];
 #pragma unroll
-            for (int J = 0; J < C::kQJ; ++J) kop[J] = *reinterpret_cast<const u32x4*>(krow + 64 * J);
-            f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int h = 0; h < 2; ++h) {
+              u32x4 kop[C::kQJ];
 #pragma unroll
-            for (int J = 0; J < C::kQJ; ++J) {
-              if constexpr (BF16) {
-                sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[J]),
-                                                             __builtin_bit_cast(bf16x8, qr[J]), sa, 0, 0, 0);
-              } else {
+              for (int J = 0; J < C::kQJ; ++J)
+                kop[J] = *reinterpret_cast<const u32x4*>(krow + h * bstride + 64 * J);
+              sa[h] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                  sa = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kop[J][e]), __uint_as_float(qr[J][e]),
-                                                            sa, 0, 0, 0);
+              for (int J = 0; J < C::kQJ; ++J) {
+                if constexpr (BF16) {
+                  sa[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[J]),
+                                                                  __builtin_bit_cast(bf16x8, qr[J]), sa[h], 0, 0, 0);
+                } else {
+#pragma unroll
+                  for (int e = 0; e < 4; ++e)
+                    sa[h] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kop[J][e]),
+                                                                 __uint_as_float(qr[J][e]), sa[h], 0, 0, 0);
+                }
               }
             }
 
-            // scale, mask, online softmax
-            const bool edge = (key0 + kBlk > hi) || (key0 + kBlk - 1 > l_ctx);
-            float x[4];
+            // scale, mask, online softmax over the pair's keys
+            float x[8];
             float mx = -INFINITY;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              x[r] = sa[r] * p.sl2;
-              if (edge) {
-                const int key = key0 + 4 * lg + r;
-                if (key >= hi || key > vis) x[r] = -INFINITY;
+            for (int h = 0; h < 2; ++h) {
+              const int kbase = h == 0 ? key0 : key1;
+              const bool edge = (kbase + kBlk > hi) || (kbase + kBlk - 1 > l_ctx);
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                float xv = sa[h][r] * p.sl2;
+                if (edge) {
+                  const int key = kbase + 4 * lg + r;
+                  if (key >= hi || key > vis) xv = -INFINITY;
+                }
+                x[4 * h + r] = xv;
+                mx = fmaxf(mx, xv);
               }
-              mx = fmaxf(mx, x[r]);
             }
             mx = row_max(mx);
-            // raise the running max only when the block's max passes it by
+            // raise the running max only when the pair's max passes it by
             // more than kLazyMax; the four lanes of a row decide alike
             const bool raise = mx > m_run + kLazyMax;
             if (__any(raise)) {
@@ -680,33 +734,39 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
               m_run = m_new;
             }
             const float m_use = m_run == -INFINITY ? 0.f : m_run;
-            float pr[4];
+            float pr[8];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
+            for (int r = 0; r < 8; ++r) {
               pr[r] = __builtin_amdgcn_exp2f(x[r] - m_use);
               l_lane += pr[r];
             }
 
             // O^T += V^T P^T
             if constexpr (BF16) {
-              i16x4 pb;
-              {
-                const uint32_t p01 = pack_bf16x2(pr[0], pr[1]);
-                const uint32_t p23 = pack_bf16x2(pr[2], pr[3]);
-                pb[0] = (short)(p01 & 0xffffu);
-                pb[1] = (short)(p01 >> 16);
-                pb[2] = (short)(p23 & 0xffffu);
-                pb[3] = (short)(p23 >> 16);
+              // 32-key contraction: element e of a lane's operands is key
+              // 4 lg + e of block kb0 (e < 4) or key 4 lg + e - 4 of kb1
+              const u32x4 pb = {pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]), pack_bf16x2(pr[4], pr[5]),
+                                pack_bf16x2(pr[6], pr[7])};
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db) {
+                const i16x4 a0 = vt[db], a1 = vt[C::kDB + db];
+                const u32x4 va = {__builtin_bit_cast(uint2, a0).x, __builtin_bit_cast(uint2, a0).y,
+                                  __builtin_bit_cast(uint2, a1).x, __builtin_bit_cast(uint2, a1).y};
+                o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, va),
+                                                                __builtin_bit_cast(bf16x8, pb), o[db], 0, 0, 0);
               }
-#pragma unroll
-              for (int db = 0; db < C::kDB; ++db)
-                o[db] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vt[db], pb, o[db], 0, 0, 0);
             } else {
+              // f32: lane (lm, lg) takes V rows key + 4 lg + r at d = 16 db + lm
 #pragma unroll
-              for (int db = 0; db < C::kDB; ++db)
+              for (int h = 0; h < 2; ++h) {
+                const char* vrow = vs + (kb0 * kBlk + 4 * lg) * C::kPitch + h * bstride + 4 * lm;
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                  o[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf[4 * db + r], pr[r], o[db], 0, 0, 0);
+                for (int db = 0; db < C::kDB; ++db)
+#pragma unroll
+                  for (int r = 0; r < 4; ++r)
+                    o[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                        *reinterpret_cast<const float*>(vrow + r * C::kPitch + 64 * db), pr[4 * h + r], o[db], 0, 0, 0);
+              }
             }
           }
         }
@@ -718,89 +778,136 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         if constexpr (!kProducer) {
 #pragma unroll
           for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
+          // the copy (and its wait for the Q loads) happens here, ahead of
+          // the stores below: placed after them, the wait would cover them too
+#pragma unroll
+          for (int J = 0; J < C::kQJ; ++J) asm volatile("" : "+v"(qr[J])::"memory");
+          // the Q of the segment after next is loaded now, right after qn was
+          // read, and before this segment's stores: its wait, a segment from
+          // now, finds the stores long done
+          int v1;
+          const Cursor c1 = next_segment(cur, v, v1);
+          if (v1 < count) {
+            int v2;
+            const Cursor c2 = next_segment(c1, v1, v2);
+            if (v2 < count) load_q(c2, qn);
+          }
         }
-        // ---- merge the key-split states of each row block through LDS
-        // (pairwise tree; this tile's stage is the scratch, and the next load
-        // into it is issued only after the next iteration's barrier)
-        char* scratch = smem + st * C::kStage;
-        for (int step = 1; step < nks; step <<= 1) {
-          lds_barrier();
+        // ---- combine the key-split states of each row block in one LDS
+        // round: every wave of the row block writes its (max, sum, O) state,
+        // then each merges all of them for its own slice of d blocks and
+        // writes that slice.  This tile's stage is the scratch; the next load
+        // into it is issued only after the next iteration's barrier.
+        float fm = 0.f, fl = 0.f;   // this lane's row: max (log2 units) and sum of the merged state
+        const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
+        const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
+        if constexpr (!kProducer) {
+          fl = row_sum(l_lane);
+          fm = m_run;
+        }
+        if (nks > 1) {
+          char* scratch = smem + st * C::kStage;
+          lds_barrier();   // every consumer is done with this tile's stage
           if constexpr (!kProducer) {
-            const int region = rb + n_rbp * (kslot / (2 * step));
-            f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
-            if (active && (kslot & (2 * step - 1)) == step) {
+            if (active) {
+              const int region = rb * nks + kslot;
+              f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
 #pragma unroll
               for (int db = 0; db < C::kDB; ++db) reg[db * 64 + lane] = o[db];
               mst[region][0][lane] = m_run;
-              mst[region][1][lane] = l_lane;
+              mst[region][1][lane] = fl;
             }
           }
           lds_barrier();
           if constexpr (!kProducer) {
-            const int region = rb + n_rbp * (kslot / (2 * step));
-            const f32x4* reg = reinterpret_cast<const f32x4*>(scratch + region * (64 * D));
-            if (active && (kslot & (2 * step - 1)) == 0 && kslot + step < nks) {
-              const float mo = mst[region][0][lane];
-              const float lo2 = mst[region][1][lane];
-              const float M = fmaxf(m_run, mo);
+            if (active) {
+              // the same order of operations in every wave of the row block
+              float M = -INFINITY;
+              for (int k = 0; k < nks; ++k) M = fmaxf(M, mst[rb * nks + k][0][lane]);
               const float Mu = M == -INFINITY ? 0.f : M;
-              const float wa = __builtin_amdgcn_exp2f(m_run - Mu);
-              const float wb = __builtin_amdgcn_exp2f(mo - Mu);
-              l_lane = l_lane * wa + lo2 * wb;
+              float wk[kConsumers];
+              float L = 0.f;
 #pragma unroll
-              for (int db = 0; db < C::kDB; ++db) o[db] = o[db] * wa + reg[db * 64 + lane] * wb;
-              m_run = M;
+              for (int k = 0; k < kConsumers; ++k) {
+                if (k < nks) {
+                  wk[k] = __builtin_amdgcn_exp2f(mst[rb * nks + k][0][lane] - Mu);
+                  L += mst[rb * nks + k][1][lane] * wk[k];
+                }
+              }
+              fm = M;
+              fl = L;
+#pragma unroll
+              for (int db = 0; db < C::kDB; ++db) {
+                if (db >= d_lo && db < d_hi) {
+                  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                  for (int k = 0; k < kConsumers; ++k) {
+                    if (k < nks) {
+                      const f32x4* reg = reinterpret_cast<const f32x4*>(scratch + (rb * nks + k) * (64 * D));
+                      acc += reg[db * 64 + lane] * wk[k];
+                    }
+                  }
+                  o[db] = acc;
+                }
+              }
             }
           }
         }
 
-        // ---- write: the whole unit (final result) or a piece of it
+        // ---- this wave's slice of the result, stored in the next
+        // iteration's window: the whole unit (final result) or a piece of it
         const int unit_first = gt - j;                 // global index of the unit's tile 0
         const bool whole = seg_g == unit_first && j == n - 1;
+        pend = true;
+        pend_whole = whole;
         if constexpr (!kProducer) {
           const int slot = 2 * pid + (seg_g == g0 ? 0 : 1);
-          if (active && kslot == 0) {
-            const float l_row = row_sum(l_lane);
-            if (row_valid) {
-              const float inv = l_row > 0.f ? 1.f / l_row : 0.f;
-              const float lse_val = l_row > 0.f ? (m_run + log2f(l_row)) * kLn2 : -INFINITY;
-              if (whole) {
-                const size_t orow = (size_t)(b * p.C_max + tok) * p.Hq + kvh * g + row % g;
-                float* dst = p.out + orow * D;
-                if (lg == 0) p.lse[orow] = lse_val;
-#pragma unroll
-                for (int db = 0; db < C::kDB; ++db)
-                  *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = o[db] * inv;
-              } else {
-                // read by another workgroup, possibly on another XCD
-                const __amdgpu_buffer_rsrc_t ws_o_rsrc =
-                    __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
-                const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
-                    __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
-                const int srow = slot * p.Rcap + row;
-                if (lg == 0)
-                  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, lse_val), ws_lse_rsrc, srow * 4, 0,
-                                                        kDeviceCoherent);
-#pragma unroll
-                for (int db = 0; db < C::kDB; ++db)
-                  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, o[db] * inv), ws_o_rsrc,
-                                                         (srow * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent);
-              }
-            }
-          }
+          pend_ok = active && row_valid;
+          pend_inv = fl > 0.f ? 1.f / fl : 0.f;
+          pend_lse = fl > 0.f ? (fm + log2f(fl)) * kLn2 : -INFINITY;
+          pend_row = whole ? (b * p.C_max + tok) * p.Hq + kvh * g + row % g : slot * p.Rcap + row;
         }
         if (!whole) {
           Pub q;
           q.state = 0;
           q.unit = b * Hkv + kvh;
-          q.v = v;
-          q.old = 0;
+          q.v = v + 1;   // the iteration whose window stores it
           if (n_pub == 0) pub0 = q;
           else pub1 = q;
           ++n_pub;
         }
       }
       if (v + 1 < count) advance(cur, v);
+    }
+    // ---- the last piece of a unit merges it, now that no tile load is in
+    // flight.  Every wave takes part in the two barriers.
+    if constexpr (!kProducer) {
+      if (ctid == 0) {
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const Pub& q = k == 0 ? pub0 : pub1;
+          int flag = 0;
+          if (q.state == 1) {
+            int uf, un;
+            unit_tiles(q.unit, uf, un);
+            const int np = sc.owner(uf + un - 1) - sc.owner(uf) + 1;   // pieces of the unit
+            flag = (k == 0 ? cnt0 : cnt1) + 1 == np ? 1 : 0;
+          }
+          sh_flag[k] = flag;
+        }
+      }
+    }
+    lds_barrier();
+    if constexpr (!kProducer) {
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        if (sh_flag[k]) {
+          const int unit = k == 0 ? pub0.unit : pub1.unit;
+          int uf, un;
+          unit_tiles(unit, uf, un);
+          merge_unit<D>(p, sc, seqs, ctid, unit, uf, un);
+        }
+      }
     }
   };
   if (producer) run(std::true_type{});
