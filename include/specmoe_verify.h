@@ -148,7 +148,7 @@ size_t specmoe_verify_attn_workspace_bytes(const specmoe_verify_desc* desc);
 int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, void* stream,
                                        const specmoe_verify_desc* desc);
 
-/* Keys per tile for `desc`'s dtype and D (16 KB of K rows).  Negative status
+/* Keys per tile for `desc`'s dtype and D (32 KB of K rows).  Negative status
  * for an invalid dtype or D. */
 int32_t specmoe_verify_attn_key_tile(const specmoe_verify_desc* desc);
 

@@ -116,10 +116,10 @@ def test_workspace_contract(lib):
 
 
 def test_key_tile(lib):
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc())) == 64    # 16 KB of bf16 D=128 rows
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=64))) == 128
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=64))) == 64
-    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=128))) == 32
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc())) == 128    # 32 KB of bf16 D=128 rows
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=64))) == 256
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=64))) == 128
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=128))) == 64
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=80))) == -4
 
 

@@ -175,10 +175,11 @@ EDGE = {
     "bf16_d64": (3, 16, 4, 64, "bf16", [500, 260, 1], [5, 3, 5], 5),
     "f32_d128": (2, 8, 2, 128, "f32", [300, 77], [4, 2], 4),
     "f32_d64_many": (3, 12, 3, 64, "f32", [1000, 5, 640], [3, 8, 1], 8),
-    # chunks longer than a key tile: some tiles (and pieces) hold no key that
-    # an early row of the chunk may see
-    "f32_chunk_longer_than_tile": (2, 4, 4, 128, "f32", [100, 5], [40, 37], 40),
-    "bf16_chunk_longer_than_tile": (2, 2, 2, 128, "bf16", [50, 300], [128, 100], 128),
+    # chunks longer than a key tile (f32, D=128: 64-key tiles): some tiles
+    # (and pieces) hold no key that an early row of the chunk may see
+    "f32_chunk_longer_than_tile": (2, 4, 4, 128, "f32", [100, 5], [100, 70], 100),
+    # bf16, D=128: a 128-key chunk fills a whole tile
+    "bf16_chunk_fills_tile": (2, 2, 2, 128, "bf16", [50, 300], [128, 100], 128),
 }
 
 
