@@ -55,9 +55,9 @@ constexpr int kConsumers = 8;                 // waves that compute
 constexpr int kWaves = kProducers + kConsumers;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kCThreads = 64 * kConsumers;
-constexpr int kStages = 2;                    // LDS ring of staged tiles
+constexpr int kStages = 2;                    // LDS stages: one per producer pair
 constexpr int kHalf = 32768;                  // K bytes (and V bytes) of one tile
-constexpr int kMaxDma = 9;                    // DMA instructions per producer wave and K (or V) tile, at most
+constexpr int kMaxDma = 18;                   // DMA instructions per producer wave and K (or V) tile, at most
 constexpr int kBlk = 16;                      // keys (and query rows) per MFMA block
 constexpr int kMaxRows = 128;                 // row blocks per unit <= 8
 constexpr int kDefaultGrid = 256;             // persistent workgroups: one per CU of an MI355X
@@ -115,18 +115,32 @@ struct Cfg {
   static constexpr int kNKB = kTileKeys / kBlk;             // 16-key blocks per tile
   static constexpr int kDB = D / 16;                        // 16-wide d blocks of O^T
   static constexpr int kQJ = kChunks / 4;                   // 16-byte Q chunks per lane
-  static_assert(kInst <= kProducers * kMaxDma, "DMA instructions per producer wave");
+  static_assert(kInst <= 2 * kMaxDma, "DMA instructions per producer wave");
   static_assert(kStages * kStage + 12 * 1024 + 256 <= 160 * 1024, "LDS budget");
   static_assert(kConsumers * 64 * D <= kStage, "key-split merge scratch fits in a stage");
   static_assert(kNKB >= 2, "key blocks are processed in pairs");
 };
 
-// Workgroup barrier that waits only for this wave's LDS operations.  A
-// __syncthreads() also waits for every outstanding direct-to-LDS load (its
-// release fence covers them), which would drain the tile pipeline at every
-// barrier; tile data is handed over by the producers' explicit waits instead.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+// Hand-offs between the waves of a workgroup go through LDS counters that
+// only grow: a wave adds one when it has done its part, and a waiting wave
+// polls until the counter reaches the total it needs.  The wait is bounded
+// (about 0.1 s of polling), so that a broken hand-off ends the kernel with
+// wrong results instead of hanging the GPU.
+constexpr int kSpinLimit = 1 << 21;
+__device__ __forceinline__ void wait_count(int* c, int target) {
+  for (int spin = 0; spin < kSpinLimit; ++spin) {
+    if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) >= target)
+      break;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  asm volatile("" ::: "memory");
+}
+// Count this wave once, after all of its earlier LDS operations (LDS serves
+// a wave's operations in order).
+__device__ __forceinline__ void signal_count(int* c) {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  if ((threadIdx.x & 63) == 0) __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  asm volatile("" ::: "memory");
 }
 
 // Max and sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 that hold one
@@ -277,6 +291,9 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   __shared__ float mst[kConsumers][2][64];   // key-split merge: row max and row sum of each wave
   __shared__ int wave_sum[kWaves];
   __shared__ int sh_flag[2];              // "this piece completed its unit", for the two pieces
+  __shared__ int full_cnt[kStages];       // producer waves whose loads of the stage's tile have landed
+  __shared__ int empty_cnt[kStages];      // consumer waves done with the stage's tile
+  __shared__ int cb_cnt;                  // consumer waves that reached a consumer barrier
 
   const int pid = blockIdx.x;
   const int tid = threadIdx.x;
@@ -307,6 +324,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     if (lane >= off) incl += y;
   }
   if (lane == 63) wave_sum[wave] = incl;
+  if (tid < kStages) {
+    full_cnt[tid] = 0;
+    empty_cnt[tid] = 0;
+  }
+  if (tid == 0) cb_cnt = 0;
   __syncthreads();
   int before = 0, total = 0;
 #pragma unroll
@@ -417,17 +439,13 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // ---- producers: K/V tile of cursor cu straight from HBM into stage st.
   // Each 64-lane load fills 64 consecutive 16-byte LDS slots (1 KB of
   // consecutive cache rows with their pad slots); a pad lane re-reads a chunk
-  // of its own row, and rows past the end of a partial tile re-read the
-  // tile's last row, so every slot holds finite data from cache lines the
-  // tile reads anyway.  Producer wave w issues the K and V instructions
-  // w, w + 4, ...
-  int drow[kMaxDma], dch[kMaxDma];
-#pragma unroll
-  for (int k = 0; k < kMaxDma; ++k) {
-    const int sl = 64 * (wave + kProducers * k) + lane;
-    drow[k] = sl / C::kSlots;
-    dch[k] = min(sl % C::kSlots, C::kChunks - 1);
-  }
+  // of its own row, and within a partial tile the lanes past its last row
+  // re-read that row.  K loads that would start past the last row are not
+  // issued: those slots keep whatever an earlier tile or merge left there,
+  // and the consumers mask the keys.  V rows are always loaded, so that a
+  // masked key (probability 0) always meets finite V values.  The two waves of a producer pair issue the K and V
+  // instructions of even and odd index.
+  const int pw = wave & 1;
   auto dma = [&](const Cursor& cu, int st) {
     const int T = seq_T(cu.s);
     const int hi = T - (seq_tiles<C>(cu.s) - 1 - cu.j) * C::kTileKeys;
@@ -441,18 +459,22 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     char* vl = kl + C::kLdsHalf;
 #pragma unroll
     for (int k = 0; k < kMaxDma; ++k) {
-      const int i = wave + kProducers * k;
-      if (i < C::kInst) {
-        const uint32_t off = (uint32_t)min(drow[k], last) * C::kRowBytes + 16u * dch[k];
-        if (64 * i + lane < C::kTileKeys * C::kSlots) {
+      const int i = pw + 2 * k;
+      const int sl = 64 * i + lane;
+      if (i < C::kInst && sl < C::kTileKeys * C::kSlots) {
+        const int drow = sl / C::kSlots;
+        const int dch = min(sl - drow * C::kSlots, C::kChunks - 1);
+        const uint32_t off = (uint32_t)min(drow, last) * C::kRowBytes + 16u * dch;
+        // a K load whose first row is past the tile's keys is skipped: those
+        // scores are masked whatever the slots hold
+        if ((64 * i) / C::kSlots <= last)
           __builtin_amdgcn_global_load_lds(kp + off, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
                                            0);
-          __builtin_amdgcn_global_load_lds(vp + off, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0,
-                                           0);
-        }
+        __builtin_amdgcn_global_load_lds(vp + off, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0, 0);
       }
     }
   };
+
 
   // ---- consumer roles for the unit of cursor cu.  Rows are cut into
   // n_rb 16-row blocks (n_rbp = n_rb rounded up to a power of two); consumer
@@ -497,421 +519,402 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   };
 
   // Publication of pieces (at most two per workgroup: its first and last
-  // segment).  A piece's stores are issued in the window after its segment;
-  // two iterations later the consumers wait for them (their own wait, which
-  // no tile load shares) and the piece is counted on its unit's arrival
-  // counter.  The counts are read back after the loop, where the last piece
-  // of a unit merges it.  The loop runs idle iterations after the last tile
-  // until every piece is counted.
+  // segment).  Two tiles after a piece's stores, the consumers wait for them
+  // (their own wait, which no tile load shares) and the piece is counted on
+  // its unit's arrival counter.  The counts are read back after the loop,
+  // where the last piece of a unit merges it.  The loop runs idle iterations
+  // after the last tile until every piece is counted.
   struct Pub {
     int state;   // 0 stored, 1 counted, 2 no piece
     int unit, v;
   };
 
-  // ---- the main loop, instantiated once for the producers and once for the
-  // consumers.  The two roles share no control flow, so the compiler's
-  // memory-wait analysis of one role adds no wait to the other; both follow
-  // the same schedule and bookkeeping, so they meet at the same barriers.
-  auto run = [&](auto role) {
-    constexpr bool kProducer = decltype(role)::value;
-    // per-segment state of a consumer lane: O^T blocks, running max (log2
-    // units, the same in the four lanes of a row), this lane's share of the
-    // row sum, and the Q operand of this unit and of the next
-    f32x4 o[C::kDB];
-    u32x4 qr[C::kQJ], qn[C::kQJ];
+  // ---- consumers.  Per-segment state of a lane: O^T blocks, running max
+  // (log2 units, the same in the four lanes of a row), this lane's share of
+  // the row sum, and the Q operand of this unit and of the next.
+  f32x4 o[C::kDB];
 #pragma unroll
-    for (int J = 0; J < C::kQJ; ++J) qn[J] = u32x4{0u, 0u, 0u, 0u};
-    float m_run = -INFINITY, l_lane = 0.f;
-    Pub pub0 = {2, 0, 0}, pub1 = {2, 0, 0};
-    int n_pub = 0;
-    // counter values before the two pieces (consumer thread 0), read after
-    // the loop, so the atomics' returns are never waited for inside it
-    int cnt0 = 0, cnt1 = 0;
+  for (int db = 0; db < C::kDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x4 qr[C::kQJ], qn[C::kQJ];
+#pragma unroll
+  for (int J = 0; J < C::kQJ; ++J) qn[J] = u32x4{0u, 0u, 0u, 0u};
+  float m_run = -INFINITY, l_lane = 0.f;
+  Pub pub0 = {2, 0, 0}, pub1 = {2, 0, 0};
+  int n_pub = 0;
+  // counter values before the two pieces (consumer thread 0), read after
+  // the loop, so the atomics' returns are never waited for inside it
+  int cnt0 = 0, cnt1 = 0;
+  int ncb = 0;   // consumer barriers passed
+  auto cbar = [&]() {
+    ++ncb;
+    signal_count(&cb_cnt);
+    wait_count(&cb_cnt, kConsumers * ncb);
+  };
 
-    // start: the first tiles in flight, the first unit's Q
-    Cursor dcur = first;                 // cursor of the next tile to load
-    int dv = 0;                          // its position in the workgroup's order
-    if constexpr (kProducer) {
-      for (; dv < kStages - 1 && dv < count; ++dv) {
-        dma(dcur, dv);
-        if (dv + 1 < count) advance(dcur, dv);
+  // The first unit's Q goes out before any tile load, so that it does not
+  // queue behind the tiles: consumers issue it, then every wave meets at a
+  // barrier (one that does not wait for those loads), then the producers
+  // start.  It arrives through qn, so that qr is only ever written from
+  // registers and the score MFMAs never wait for a load.
+  if (!producer) load_q(first, qn);
+  asm volatile("s_barrier" ::: "memory");
+  if (producer) {
+    // Producer pair grp streams the tiles v = grp, grp + 2, ... of the
+    // workgroup's order into stage grp: it waits until all consumers have
+    // released the stage's previous tile, issues the loads, waits for its own
+    // loads to land and counts itself on the stage's fill counter.  The two
+    // pairs run independently, so one tile's loads are issued while the
+    // other's are still in flight.
+    const int grp = wave >> 1;
+    Cursor cu = first;
+    int v = grp;
+    if (grp == 1 && count > 1) advance(cu, 0);
+    for (; v < count; v += 2) {
+      if (v >= 2) wait_count(&empty_cnt[grp], kConsumers * (v >> 1));
+      dma(cu, grp);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      signal_count(&full_cnt[grp]);
+      if (v + 2 < count) {
+        advance(cu, v);
+        advance(cu, v + 1);
       }
+    }
+    return;
+  }
+#pragma unroll
+  for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
+#pragma unroll
+  for (int J = 0; J < C::kQJ; ++J) asm volatile("" : "+v"(qr[J])::"memory");
+  {
+    int v1;
+    const Cursor c1 = next_segment(first, 0, v1);
+    if (v1 < count) load_q(c1, qn);   // the second segment's Q
+  }
+  Cursor cur = first;                  // cursor of the tile being computed
+  int seg_g = g0;
+  // results of the segment that ended in the previous iteration, stored at
+  // the top of this one: o[] (this wave's d blocks), and per lane the output
+  // (or workspace) row, 1 / row sum and the row's lse
+  bool pend = false, pend_whole = false, pend_ok = false;
+  int pend_row = 0;
+  float pend_inv = 0.f, pend_lse = 0.f;
+
+  for (int v = 0;; ++v) {
+    if (v >= count && pub0.state != 0 && pub1.state != 0 && !pend) break;
+    if (pend && pend_ok) {
+      const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
+      const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
+      if (pend_whole) {
+        float* dst = p.out + (size_t)pend_row * D;
+        if (kslot == 0 && lg == 0) p.lse[pend_row] = pend_lse;
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db)
+          if (db >= d_lo && db < d_hi) *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = o[db] * pend_inv;
+      } else {
+        // read by another workgroup, possibly on another XCD
+        const __amdgpu_buffer_rsrc_t ws_o_rsrc =
+            __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
+        const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
+            __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
+        if (kslot == 0 && lg == 0)
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, pend_lse), ws_lse_rsrc, pend_row * 4, 0,
+                                                kDeviceCoherent);
+#pragma unroll
+        for (int db = 0; db < C::kDB; ++db)
+          if (db >= d_lo && db < d_hi)
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, o[db] * pend_inv), ws_o_rsrc,
+                                                   (pend_row * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent);
+      }
+    }
+    if (pend) {
+      // the next tile starts a new segment
+#pragma unroll
+      for (int db = 0; db < C::kDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    pend = false;
+    const bool due0 = pub0.state == 0 && v >= pub0.v + 2;
+    const bool due1 = pub1.state == 0 && v >= pub1.v + 2;
+    if (due0 || due1) {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's piece stores
+      Pub& q = due0 ? pub0 : pub1;
+      if (ctid == 0) {
+        const int old = __hip_atomic_fetch_add(p.counters + q.unit, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (due0) cnt0 = old;
+        else cnt1 = old;
+      }
+      q.state = 1;
+    }
+    if (v >= count) continue;
+
+    const int st = v & 1;
+    wait_count(&full_cnt[st], 2 * ((v >> 1) + 1));   // tile v is in stage st
+    const int b = cur.b, kvh = cur.kvh, j = cur.j;
+    const uint32_t s = cur.s;
+    const int n = seq_tiles<C>(s);
+    const int gt = tile_at(v);
+    const bool seg_first = v == 0 || v == nL || j == 0;
+    const bool seg_last = v == count - 1 || v + 1 == nL || j == n - 1;
+    if (seg_first) {
+      roles(cur);
+      m_run = -INFINITY;
+      l_lane = 0.f;
+      seg_g = gt;
+    }
+
+    {
+      const char* ks = smem + st * C::kStage;
+      const char* vs = ks + C::kLdsHalf;
+      const int T = seq_T(s);
+      const int hi = T - (n - 1 - j) * C::kTileKeys;
+      const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
+      const int nk = hi - lo;
+      // Key blocks kb0 and kb1 = kb0 + nks of the tile form a pair: two
+      // independent score chains, one softmax step over their 8 keys per
+      // lane, and (bf16) one 32-key P V contraction per d block.  A block
+      // past the tile's keys reads staged rows that hold finite data and
+      // is masked like any key >= hi.
+      // (an inactive wave runs no pair)
+      for (int kb0 = active ? kslot : C::kNKB; kb0 < C::kNKB; kb0 += 2 * nks) {
+        if (kb0 * kBlk >= nk) break;
+        const int key0 = lo + kb0 * kBlk;
+        const int key1 = key0 + nks * kBlk;
+        const int bstride = nks * kBlk * C::kPitch;   // LDS bytes from block kb0 to kb1
+        // S^T = K Q^T for 16 keys x 16 rows per block; lane (row lm,
+        // quarter lg) gets the keys key + 4 lg + r, r = 0..3
+        const char* krow = ks + (kb0 * kBlk + lm) * C::kPitch + 16 * lg;
+        f32x4 sa[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          u32x4 kop[C::kQJ];
+#pragma unroll
+          for (int J = 0; J < C::kQJ; ++J)
+            kop[J] = *reinterpret_cast<const u32x4*>(krow + h * bstride + 64 * J);
+          sa[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int J = 0; J < C::kQJ; ++J) {
+            if constexpr (BF16) {
+              sa[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[J]),
+                                                              __builtin_bit_cast(bf16x8, qr[J]), sa[h], 0, 0, 0);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                sa[h] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kop[J][e]),
+                                                             __uint_as_float(qr[J][e]), sa[h], 0, 0, 0);
+            }
+          }
+        }
+
+        __builtin_amdgcn_sched_barrier(0);
+
+        // V^T operands, read once the score MFMAs have taken their K
+        // operands (fewer live registers; the reads overlap the MFMAs and the
+        // softmax step): lane
+        // (lm, lg) needs V rows key + 4 lg + e, e = 0..3, at d = 16 db + lm
+        // of both blocks.  bf16: one transposed LDS read per block and d
+        // block, in which lane t of the 16-lane group lg points at row
+        // key + 4 lg + t / 4, columns 16 db + 4 (t % 4) .. + 3.
+        i16x4 vt[BF16 ? 2 * C::kDB : 1];
+        if constexpr (BF16) {
+          typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+          const char* vrow = vs + (kb0 * kBlk + 4 * lg + (lm >> 2)) * C::kPitch + 8 * (lm & 3);
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int db = 0; db < C::kDB; ++db)
+              vt[h * C::kDB + db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                  (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + h * bstride + 32 * db));
+        }
+
+        // scale, mask, online softmax over the pair's keys
+        float x[8];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int kbase = h == 0 ? key0 : key1;
+          const bool edge = (kbase + kBlk > hi) || (kbase + kBlk - 1 > l_ctx);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            float xv = sa[h][r] * p.sl2;
+            if (edge) {
+              const int key = kbase + 4 * lg + r;
+              if (key >= hi || key > vis) xv = -INFINITY;
+            }
+            x[4 * h + r] = xv;
+            mx = fmaxf(mx, xv);
+          }
+        }
+        mx = row_max(mx);
+        // raise the running max only when the pair's max passes it by
+        // more than kLazyMax; the four lanes of a row decide alike
+        const bool raise = mx > m_run + kLazyMax;
+        if (__any(raise)) {
+          const float m_new = raise ? mx : m_run;
+          const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
+          l_lane *= alpha;
+#pragma unroll
+          for (int db = 0; db < C::kDB; ++db) o[db] *= alpha;
+          m_run = m_new;
+        }
+        const float m_use = m_run == -INFINITY ? 0.f : m_run;
+        float pr[8];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          pr[r] = __builtin_amdgcn_exp2f(x[r] - m_use);
+          l_lane += pr[r];
+        }
+
+        // O^T += V^T P^T
+        if constexpr (BF16) {
+          // 32-key contraction: element e of a lane's operands is key
+          // 4 lg + e of block kb0 (e < 4) or key 4 lg + e - 4 of kb1
+          const u32x4 pb = {pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]), pack_bf16x2(pr[4], pr[5]),
+                            pack_bf16x2(pr[6], pr[7])};
+#pragma unroll
+          for (int db = 0; db < C::kDB; ++db) {
+            const i16x4 a0 = vt[db], a1 = vt[C::kDB + db];
+            const u32x4 va = {__builtin_bit_cast(uint2, a0).x, __builtin_bit_cast(uint2, a0).y,
+                              __builtin_bit_cast(uint2, a1).x, __builtin_bit_cast(uint2, a1).y};
+            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, va),
+                                                            __builtin_bit_cast(bf16x8, pb), o[db], 0, 0, 0);
+          }
+        } else {
+          // f32: lane (lm, lg) takes V rows key + 4 lg + r at d = 16 db + lm
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const char* vrow = vs + (kb0 * kBlk + 4 * lg) * C::kPitch + h * bstride + 4 * lm;
+#pragma unroll
+            for (int db = 0; db < C::kDB; ++db)
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                o[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                    *reinterpret_cast<const float*>(vrow + r * C::kPitch + 64 * db), pr[4 * h + r], o[db], 0, 0, 0);
+          }
+        }
+      }
+    }
+
+    if (!seg_last) {
+      signal_count(&empty_cnt[st]);   // done with stage st
     } else {
-      // through qn, so that qr is only ever written from registers and the
-      // score MFMAs never wait for a load
-      load_q(first, qn);
+      // the next segment's Q (loaded a segment ago) becomes current before
+      // this segment's results are stored, so its wait covers no store
 #pragma unroll
       for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
 #pragma unroll
       for (int J = 0; J < C::kQJ; ++J) asm volatile("" : "+v"(qr[J])::"memory");
-      int v1;
-      const Cursor c1 = next_segment(first, 0, v1);
-      if (v1 < count) load_q(c1, qn);   // the second segment's Q
-    }
-    Cursor cur = first;                  // cursor of the tile being computed
-    int seg_g = g0;
-    // results of the segment that ended in the previous iteration, stored in
-    // this iteration's window: o[] (this wave's d blocks), and per lane the
-    // output (or workspace) row, 1 / row sum and the row's lse
-    bool pend = false, pend_whole = false, pend_ok = false;
-    int pend_row = 0;
-    float pend_inv = 0.f, pend_lse = 0.f;
-
-    for (int v = 0;; ++v) {
-      if (v >= count && pub0.state != 0 && pub1.state != 0 && !pend) break;
-      const int st = v % kStages;
-      const bool due0 = pub0.state == 0 && v >= pub0.v + 2;
-      const bool due1 = pub1.state == 0 && v >= pub1.v + 2;
-      if constexpr (kProducer) {
-        // this producer's loads of tile v have landed in LDS (with two
-        // stages it is the only tile in flight)
-        if (v < count) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      } else {
-        if (due0 || due1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's piece stores
-      }
-      lds_barrier();   // tile v is in LDS; every wave is done with tile v - 1 and its merges
-
-      // ---- window for the consumers' own global memory operations: the
-      // stores of the segment that ended in the previous iteration and the
-      // count of a stored piece.  The next tile's loads are issued only after
-      // it (a second barrier), so these operations do not queue behind a
-      // tile's worth of loads in the CU's memory pipeline.
-      const bool window = pend || due0 || due1;
-      if constexpr (!kProducer) {
-        if (pend && pend_ok) {
-          const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
-          const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
-          if (pend_whole) {
-            float* dst = p.out + (size_t)pend_row * D;
-            if (kslot == 0 && lg == 0) p.lse[pend_row] = pend_lse;
-#pragma unroll
-            for (int db = 0; db < C::kDB; ++db)
-              if (db >= d_lo && db < d_hi) *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = o[db] * pend_inv;
-          } else {
-            // read by another workgroup, possibly on another XCD
-            const __amdgpu_buffer_rsrc_t ws_o_rsrc =
-                __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
-            const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
-                __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
-            if (kslot == 0 && lg == 0)
-              __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, pend_lse), ws_lse_rsrc, pend_row * 4, 0,
-                                                    kDeviceCoherent);
-#pragma unroll
-            for (int db = 0; db < C::kDB; ++db)
-              if (db >= d_lo && db < d_hi)
-                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, o[db] * pend_inv), ws_o_rsrc,
-                                                       (pend_row * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent);
-          }
+      // the Q of the segment after next is loaded now, right after qn was
+      // read, and before this segment's stores
+      {
+        int v1;
+        const Cursor c1 = next_segment(cur, v, v1);
+        if (v1 < count) {
+          int v2;
+          const Cursor c2 = next_segment(c1, v1, v2);
+          if (v2 < count) load_q(c2, qn);
         }
       }
-      pend = false;
-      if (due0 || due1) {
-        Pub& q = due0 ? pub0 : pub1;
-        if constexpr (!kProducer) {
-          if (ctid == 0) {
-            const int old = __hip_atomic_fetch_add(p.counters + q.unit, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            if (due0) cnt0 = old;
-            else cnt1 = old;
-          }
-        }
-        q.state = 1;
-      }
-      if (window) lds_barrier();
-      if constexpr (kProducer) {
-        if (dv < count) {
-          dma(dcur, dv % kStages);
-          if (dv + 1 < count) advance(dcur, dv);
-          ++dv;
-        }
-      }
-      if (v >= count) continue;
-
-      const int b = cur.b, kvh = cur.kvh, j = cur.j;
-      const uint32_t s = cur.s;
-      const int n = seq_tiles<C>(s);
-      const int gt = tile_at(v);
-      const bool seg_first = v == 0 || v == nL || j == 0;
-      const bool seg_last = v == count - 1 || v + 1 == nL || j == n - 1;
-      if (seg_first) {
-        roles(cur);
-        if constexpr (!kProducer) {
-#pragma unroll
-          for (int db = 0; db < C::kDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
-          m_run = -INFINITY;
-          l_lane = 0.f;
-        }
-        seg_g = gt;
-      }
-
-      if constexpr (!kProducer) {
+      // ---- combine the key-split states of each row block in one LDS
+      // round: every wave of the row block writes its (max, sum, O) state,
+      // then each merges all of them for its own slice of d blocks.  This
+      // tile's stage is the scratch; it is released only afterwards.
+      float fm = m_run, fl = row_sum(l_lane);   // this lane's row: max (log2 units) and sum
+      const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
+      const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
+      if (nks > 1) {
+        char* scratch = smem + st * C::kStage;
+        cbar();   // every consumer is done with this tile's stage
         if (active) {
-          const char* ks = smem + st * C::kStage;
-          const char* vs = ks + C::kLdsHalf;
-          const int T = seq_T(s);
-          const int hi = T - (n - 1 - j) * C::kTileKeys;
-          const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
-          const int nk = hi - lo;
-          // Key blocks kb0 and kb1 = kb0 + nks of the tile form a pair: two
-          // independent score chains, one softmax step over their 8 keys per
-          // lane, and (bf16) one 32-key P V contraction per d block.  A block
-          // past the tile's keys reads staged rows that hold finite data and
-          // is masked like any key >= hi.
-          for (int kb0 = kslot; kb0 < C::kNKB; kb0 += 2 * nks) {
-            if (kb0 * kBlk >= nk) break;
-            const int key0 = lo + kb0 * kBlk;
-            const int key1 = key0 + nks * kBlk;
-            const int bstride = nks * kBlk * C::kPitch;   // LDS bytes from block kb0 to kb1
-            // V^T operands first (they do not depend on the scores): lane
-            // (lm, lg) needs V rows key + 4 lg + e, e = 0..3, at d = 16 db + lm
-            // of both blocks.  bf16: one transposed LDS read per block and d
-            // block, in which lane t of the 16-lane group lg points at row
-            // key + 4 lg + t / 4, columns 16 db + 4 (t % 4) .. + 3.
-            i16x4 vt[BF16 ? 2 * C::kDB : 1];
-            if constexpr (BF16) {
-              typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-              const char* vrow = vs + (kb0 * kBlk + 4 * lg + (lm >> 2)) * C::kPitch + 8 * (lm & 3);
+          const int region = rb * nks + kslot;
+          f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
 #pragma unroll
-              for (int h = 0; h < 2; ++h)
+          for (int db = 0; db < C::kDB; ++db) reg[db * 64 + lane] = o[db];
+          mst[region][0][lane] = m_run;
+          mst[region][1][lane] = fl;
+        }
+        cbar();
+        if (active) {
+          // the same order of operations in every wave of the row block
+          float M = -INFINITY;
+          for (int k = 0; k < nks; ++k) M = fmaxf(M, mst[rb * nks + k][0][lane]);
+          const float Mu = M == -INFINITY ? 0.f : M;
+          float wk[kConsumers];
+          float L = 0.f;
 #pragma unroll
-                for (int db = 0; db < C::kDB; ++db)
-                  vt[h * C::kDB + db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                      (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + h * bstride + 32 * db));
-            }
-
-            // S^T = K Q^T for 16 keys x 16 rows per block; lane (row lm,
-            // quarter lg) gets the keys key + 4 lg + r, r = 0..3
-            const char* krow = ks + (kb0 * kBlk + lm) * C::kPitch + 16 * lg;
-            f32x4 sa[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              u32x4 kop[C::kQJ];
-#pragma unroll
-              for (int J = 0; J < C::kQJ; ++J)
-                kop[J] = *reinterpret_cast<const u32x4*>(krow + h * bstride + 64 * J);
-              sa[h] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-              for (int J = 0; J < C::kQJ; ++J) {
-                if constexpr (BF16) {
-                  sa[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[J]),
-                                                                  __builtin_bit_cast(bf16x8, qr[J]), sa[h], 0, 0, 0);
-                } else {
-#pragma unroll
-                  for (int e = 0; e < 4; ++e)
-                    sa[h] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kop[J][e]),
-                                                                 __uint_as_float(qr[J][e]), sa[h], 0, 0, 0);
-                }
-              }
-            }
-
-            // scale, mask, online softmax over the pair's keys
-            float x[8];
-            float mx = -INFINITY;
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              const int kbase = h == 0 ? key0 : key1;
-              const bool edge = (kbase + kBlk > hi) || (kbase + kBlk - 1 > l_ctx);
-#pragma unroll
-              for (int r = 0; r < 4; ++r) {
-                float xv = sa[h][r] * p.sl2;
-                if (edge) {
-                  const int key = kbase + 4 * lg + r;
-                  if (key >= hi || key > vis) xv = -INFINITY;
-                }
-                x[4 * h + r] = xv;
-                mx = fmaxf(mx, xv);
-              }
-            }
-            mx = row_max(mx);
-            // raise the running max only when the pair's max passes it by
-            // more than kLazyMax; the four lanes of a row decide alike
-            const bool raise = mx > m_run + kLazyMax;
-            if (__any(raise)) {
-              const float m_new = raise ? mx : m_run;
-              const float alpha = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
-              l_lane *= alpha;
-#pragma unroll
-              for (int db = 0; db < C::kDB; ++db) o[db] *= alpha;
-              m_run = m_new;
-            }
-            const float m_use = m_run == -INFINITY ? 0.f : m_run;
-            float pr[8];
-#pragma unroll
-            for (int r = 0; r < 8; ++r) {
-              pr[r] = __builtin_amdgcn_exp2f(x[r] - m_use);
-              l_lane += pr[r];
-            }
-
-            // O^T += V^T P^T
-            if constexpr (BF16) {
-              // 32-key contraction: element e of a lane's operands is key
-              // 4 lg + e of block kb0 (e < 4) or key 4 lg + e - 4 of kb1
-              const u32x4 pb = {pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]), pack_bf16x2(pr[4], pr[5]),
-                                pack_bf16x2(pr[6], pr[7])};
-#pragma unroll
-              for (int db = 0; db < C::kDB; ++db) {
-                const i16x4 a0 = vt[db], a1 = vt[C::kDB + db];
-                const u32x4 va = {__builtin_bit_cast(uint2, a0).x, __builtin_bit_cast(uint2, a0).y,
-                                  __builtin_bit_cast(uint2, a1).x, __builtin_bit_cast(uint2, a1).y};
-                o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, va),
-                                                                __builtin_bit_cast(bf16x8, pb), o[db], 0, 0, 0);
-              }
-            } else {
-              // f32: lane (lm, lg) takes V rows key + 4 lg + r at d = 16 db + lm
-#pragma unroll
-              for (int h = 0; h < 2; ++h) {
-                const char* vrow = vs + (kb0 * kBlk + 4 * lg) * C::kPitch + h * bstride + 4 * lm;
-#pragma unroll
-                for (int db = 0; db < C::kDB; ++db)
-#pragma unroll
-                  for (int r = 0; r < 4; ++r)
-                    o[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                        *reinterpret_cast<const float*>(vrow + r * C::kPitch + 64 * db), pr[4 * h + r], o[db], 0, 0, 0);
-              }
+          for (int k = 0; k < kConsumers; ++k) {
+            if (k < nks) {
+              wk[k] = __builtin_amdgcn_exp2f(mst[rb * nks + k][0][lane] - Mu);
+              L += mst[rb * nks + k][1][lane] * wk[k];
             }
           }
-        }
-      }
-
-      if (seg_last) {
-        // the next segment's Q (loaded a segment ago) becomes current before
-        // this segment's results are stored, so its wait covers no store
-        if constexpr (!kProducer) {
+          fm = M;
+          fl = L;
 #pragma unroll
-          for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
-          // the copy (and its wait for the Q loads) happens here, ahead of
-          // the stores below: placed after them, the wait would cover them too
-#pragma unroll
-          for (int J = 0; J < C::kQJ; ++J) asm volatile("" : "+v"(qr[J])::"memory");
-          // the Q of the segment after next is loaded now, right after qn was
-          // read, and before this segment's stores: its wait, a segment from
-          // now, finds the stores long done
-          int v1;
-          const Cursor c1 = next_segment(cur, v, v1);
-          if (v1 < count) {
-            int v2;
-            const Cursor c2 = next_segment(c1, v1, v2);
-            if (v2 < count) load_q(c2, qn);
-          }
-        }
-        // ---- combine the key-split states of each row block in one LDS
-        // round: every wave of the row block writes its (max, sum, O) state,
-        // then each merges all of them for its own slice of d blocks and
-        // writes that slice.  This tile's stage is the scratch; the next load
-        // into it is issued only after the next iteration's barrier.
-        float fm = 0.f, fl = 0.f;   // this lane's row: max (log2 units) and sum of the merged state
-        const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
-        const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
-        if constexpr (!kProducer) {
-          fl = row_sum(l_lane);
-          fm = m_run;
-        }
-        if (nks > 1) {
-          char* scratch = smem + st * C::kStage;
-          lds_barrier();   // every consumer is done with this tile's stage
-          if constexpr (!kProducer) {
-            if (active) {
-              const int region = rb * nks + kslot;
-              f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
-#pragma unroll
-              for (int db = 0; db < C::kDB; ++db) reg[db * 64 + lane] = o[db];
-              mst[region][0][lane] = m_run;
-              mst[region][1][lane] = fl;
-            }
-          }
-          lds_barrier();
-          if constexpr (!kProducer) {
-            if (active) {
-              // the same order of operations in every wave of the row block
-              float M = -INFINITY;
-              for (int k = 0; k < nks; ++k) M = fmaxf(M, mst[rb * nks + k][0][lane]);
-              const float Mu = M == -INFINITY ? 0.f : M;
-              float wk[kConsumers];
-              float L = 0.f;
+          for (int db = 0; db < C::kDB; ++db) {
+            if (db >= d_lo && db < d_hi) {
+              f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
               for (int k = 0; k < kConsumers; ++k) {
                 if (k < nks) {
-                  wk[k] = __builtin_amdgcn_exp2f(mst[rb * nks + k][0][lane] - Mu);
-                  L += mst[rb * nks + k][1][lane] * wk[k];
+                  const f32x4* reg = reinterpret_cast<const f32x4*>(scratch + (rb * nks + k) * (64 * D));
+                  acc += reg[db * 64 + lane] * wk[k];
                 }
               }
-              fm = M;
-              fl = L;
-#pragma unroll
-              for (int db = 0; db < C::kDB; ++db) {
-                if (db >= d_lo && db < d_hi) {
-                  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                  for (int k = 0; k < kConsumers; ++k) {
-                    if (k < nks) {
-                      const f32x4* reg = reinterpret_cast<const f32x4*>(scratch + (rb * nks + k) * (64 * D));
-                      acc += reg[db * 64 + lane] * wk[k];
-                    }
-                  }
-                  o[db] = acc;
-                }
-              }
+              o[db] = acc;
             }
           }
         }
+      }
+      signal_count(&empty_cnt[st]);   // done with stage st (and its scratch use)
 
-        // ---- this wave's slice of the result, stored in the next
-        // iteration's window: the whole unit (final result) or a piece of it
-        const int unit_first = gt - j;                 // global index of the unit's tile 0
-        const bool whole = seg_g == unit_first && j == n - 1;
-        pend = true;
-        pend_whole = whole;
-        if constexpr (!kProducer) {
-          const int slot = 2 * pid + (seg_g == g0 ? 0 : 1);
-          pend_ok = active && row_valid;
-          pend_inv = fl > 0.f ? 1.f / fl : 0.f;
-          pend_lse = fl > 0.f ? (fm + log2f(fl)) * kLn2 : -INFINITY;
-          pend_row = whole ? (b * p.C_max + tok) * p.Hq + kvh * g + row % g : slot * p.Rcap + row;
-        }
-        if (!whole) {
-          Pub q;
-          q.state = 0;
-          q.unit = b * Hkv + kvh;
-          q.v = v + 1;   // the iteration whose window stores it
-          if (n_pub == 0) pub0 = q;
-          else pub1 = q;
-          ++n_pub;
-        }
+      // ---- this wave's slice of the result, stored at the top of the next
+      // iteration: the whole unit (final result) or a piece of it
+      const int unit_first = gt - j;                 // global index of the unit's tile 0
+      const bool whole = seg_g == unit_first && j == n - 1;
+      pend = true;
+      pend_whole = whole;
+      pend_ok = active && row_valid;
+      pend_inv = fl > 0.f ? 1.f / fl : 0.f;
+      pend_lse = fl > 0.f ? (fm + log2f(fl)) * kLn2 : -INFINITY;
+      pend_row = whole ? (b * p.C_max + tok) * p.Hq + kvh * g + row % g : (2 * pid + (seg_g == g0 ? 0 : 1)) * p.Rcap + row;
+      if (!whole) {
+        Pub q;
+        q.state = 0;
+        q.unit = b * Hkv + kvh;
+        q.v = v + 1;   // the iteration that stores it
+        if (n_pub == 0) pub0 = q;
+        else pub1 = q;
+        ++n_pub;
       }
-      if (v + 1 < count) advance(cur, v);
     }
-    // ---- the last piece of a unit merges it, now that no tile load is in
-    // flight.  Every wave takes part in the two barriers.
-    if constexpr (!kProducer) {
-      if (ctid == 0) {
+    if (v + 1 < count) advance(cur, v);
+  }
+
+  // ---- the last piece of a unit merges it, now that this workgroup's tiles
+  // are done
+  if (ctid == 0) {
 #pragma unroll
-        for (int k = 0; k < 2; ++k) {
-          const Pub& q = k == 0 ? pub0 : pub1;
-          int flag = 0;
-          if (q.state == 1) {
-            int uf, un;
-            unit_tiles(q.unit, uf, un);
-            const int np = sc.owner(uf + un - 1) - sc.owner(uf) + 1;   // pieces of the unit
-            flag = (k == 0 ? cnt0 : cnt1) + 1 == np ? 1 : 0;
-          }
-          sh_flag[k] = flag;
-        }
+    for (int k = 0; k < 2; ++k) {
+      const Pub& q = k == 0 ? pub0 : pub1;
+      int flag = 0;
+      if (q.state == 1) {
+        int uf, un;
+        unit_tiles(q.unit, uf, un);
+        const int np = sc.owner(uf + un - 1) - sc.owner(uf) + 1;   // pieces of the unit
+        flag = (k == 0 ? cnt0 : cnt1) + 1 == np ? 1 : 0;
       }
+      sh_flag[k] = flag;
     }
-    lds_barrier();
-    if constexpr (!kProducer) {
+  }
+  cbar();
 #pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        if (sh_flag[k]) {
-          const int unit = k == 0 ? pub0.unit : pub1.unit;
-          int uf, un;
-          unit_tiles(unit, uf, un);
-          merge_unit<D>(p, sc, seqs, ctid, unit, uf, un);
-        }
-      }
+  for (int k = 0; k < 2; ++k) {
+    if (sh_flag[k]) {
+      const int unit = k == 0 ? pub0.unit : pub1.unit;
+      int uf, un;
+      unit_tiles(unit, uf, un);
+      merge_unit<D>(p, sc, seqs, ctid, unit, uf, un);
     }
-  };
-  if (producer) run(std::true_type{});
-  else run(std::false_type{});
+  }
 }
 
 // Zero the per-unit counters of a workspace.
