@@ -9,7 +9,7 @@
 //     query heads that share the KV head form the unit's R_b = c_b*g query
 //     rows, cut into 16-row blocks, so that Q K^T and P V become small dense
 //     MFMA contractions that reuse every K/V byte for all rows.
-//   * Key tiles: a unit's keys [0, T_b) are cut into tiles of 16 KB of K rows
+//   * Key tiles: a unit's keys [0, T_b) are cut into tiles of 32 KB of K rows
 //     anchored at T_b (tile n-1 = [T_b - kTileKeys, T_b)), so the chunk's own
 //     keys sit at the end of the unit's last tile.
 //   * Stream-K schedule: the tiles of all units, in unit order, form one list
@@ -19,26 +19,29 @@
 //     combined, as the paper notes for its sequence-dimension KV split
 //     (Section 5.2): each piece writes (O/l, lse) to the workspace and counts
 //     itself on an arrival counter; the last piece to arrive merges all of
-//     them with log-sum-exp weights.  A workgroup streams the cut unit at the
-//     end of its range first, so both pieces of every cut unit are done, and
-//     merged, early in the launch, while the memory pipeline keeps streaming.
+//     them with log-sum-exp weights, after its own tiles.  A workgroup streams
+//     the cut unit at the end of its range first, so both pieces of every cut
+//     unit are done early in the launch.
 //   * Warp-specialised pipeline: 4 producer waves stream K/V tiles from HBM
-//     straight into a 4-stage LDS ring with direct-to-LDS loads (one wave
-//     instruction moves 1 KB of contiguous cache rows); three tiles (96 KB)
-//     are in flight while 8 consumer waves compute on the fourth.  Only the
-//     producers issue tile loads, so a consumer's wait for its own stores or
-//     loads never drains the tile stream.  LDS rows are padded by 16 bytes,
-//     so every MFMA operand read is free of bank conflicts and all operand
-//     addresses are a per-lane base plus an immediate.
+//     straight into LDS with direct-to-LDS loads (one wave instruction moves
+//     1 KB of contiguous cache rows); 8 consumer waves compute.  The producers
+//     form two pairs, each owning one of two LDS stages; tiles and stages are
+//     handed over through LDS counters (no workgroup barrier on the tile
+//     path), so one pair's tile is in flight while the other's is computed.
+//     Only the producers issue tile loads, so a consumer's wait for its own
+//     stores or loads never drains the tile stream.  LDS rows are padded by
+//     16 bytes, so every MFMA operand read is free of bank conflicts and all
+//     operand addresses are a per-lane base plus an immediate.
 //   * Scores are formed transposed, S^T = K Q^T (keys on the MFMA M side,
 //     query rows on N), so each lane holds one query row and four keys: row
 //     statistics need two cross-lane steps, and the probabilities are already
-//     the B operand of O^T = V^T P^T.  The consumers split a tile's 16-key
-//     blocks between them; their partial (max, sum, O) states are merged
-//     through LDS at the end of each unit.
-//   * bf16 inputs use v_mfma_f32_16x16x32_bf16 for the scores and
-//     v_mfma_f32_16x16x16_bf16 for P V, with fp32 accumulation (P is rounded
-//     to bf16 for the PV product); f32 inputs use v_mfma_f32_16x16x4_f32.
+//     the B operand of O^T = V^T P^T.  A consumer wave takes two 16-key blocks
+//     of a tile; the waves that share a row block merge their partial (max,
+//     sum, O) states through LDS at the end of each unit.
+//   * bf16 inputs use v_mfma_f32_16x16x32_bf16 for the scores and for P V
+//     (one 32-key contraction over the wave's two blocks), with fp32
+//     accumulation (P is rounded to bf16 for the PV product); f32 inputs use
+//     v_mfma_f32_16x16x4_f32.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
