@@ -10,7 +10,9 @@ value = effective KV GB/s = sum_b Hkv*(l_b + c_b)*D*elt*2 / t_step, the K+V
 bytes of every valid row (the attention row of the paper's cost table,
 2*b*s*h/g elements, Section 3.2).  Input sets are rotated so that successive
 steps read different HBM addresses and the KV cannot be served from the
-256 MB Infinity Cache.
+256 MB Infinity Cache.  Before the warmup steps, steps run for --settle-ms of
+sustained load (reported as settle_steps), so that the timed steps see the
+GPU at its working clock rather than its ramp.
 """
 from __future__ import annotations
 
@@ -101,6 +103,9 @@ def main():
     ap.add_argument("--grid-blocks", type=int, default=0, help="persistent workgroups (0: library default)")
     ap.add_argument("--rotate", type=int, default=0, help="input sets (0: enough for >= 1 GB)")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work; 0 skips")
+    ap.add_argument("--settle-ms", type=float, default=200.0,
+                    help="before the warmup steps, run steps until the GPU has been busy this long "
+                         "(its clocks ramp up over the first tens of ms of sustained load); 0 skips")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MB",
                     help="instead of the benchmark, run a plain elementwise copy of MB MiB (float32 read, "
                          "float32 write) 5 times: the known byte counts calibrate the HBM traffic counters")
@@ -163,6 +168,16 @@ def main():
         pkg.verify_attn(q, k, v, ctx_d, chunk_d, w.scale, out=out, lse=lse, workspace=ws,
                         grid_blocks=args.grid_blocks, stream=stream, events=events)
 
+    # settle: sustained load until the GPU runs at its working clock (a short
+    # warmup alone measures the ramp: about 5% slower on this workload)
+    settle_steps = 0
+    torch.cuda.synchronize()
+    t_settle = time.time()
+    while (time.time() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(20):
+            step(settle_steps)
+            settle_steps += 1
+        torch.cuda.synchronize()
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -212,6 +227,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_steps": settle_steps,
         "ms_per_step": round(ms_per_step, 6),
         "higher_is_better": True,
         "scaling": "weak",

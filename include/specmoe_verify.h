@@ -80,8 +80,11 @@ typedef struct specmoe_verify_desc {
  * specmoe_verify_attn -- chunked verification attention (Section 5.1).
  *
  * Work split: the keys of every (sequence, KV head) are cut into tiles, and
- * the tiles of all of them are divided into `grid_blocks` equal contiguous
- * ranges, one per persistent workgroup.  A (sequence, KV head) whose tiles
+ * the tiles of all of them are divided into at most `grid_blocks` contiguous
+ * ranges of equal cost, one per persistent workgroup; a tile's cost grows
+ * with the query rows (c_b * Hq / Hkv) that compute on it, so with equal
+ * chunk lengths every range holds the same number of tiles (give or take
+ * one).  A (sequence, KV head) whose tiles
  * span several ranges is computed in pieces that are merged with log-sum-exp
  * weights -- the sequence-dimension KV partition of Section 5.2 -- through
  * the workspace.  The split depends only on the lengths and grid_blocks, and

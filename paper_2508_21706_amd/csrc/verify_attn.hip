@@ -13,8 +13,13 @@
 //     anchored at T_b (tile n-1 = [T_b - kTileKeys, T_b)), so the chunk's own
 //     keys sit at the end of the unit's last tile.
 //   * Stream-K schedule: the tiles of all units, in unit order, form one list
-//     cut into equal contiguous ranges, one per workgroup, so that every
-//     workgroup streams the same number of K/V bytes.  A unit cut by a range
+//     cut into contiguous ranges of equal cost, one per workgroup.  A tile's
+//     cost grows with its unit's row count (a unit with many rows computes
+//     longer on a tile than the tile takes to stream); when every unit has
+//     the same rows, every workgroup streams the same number of K/V bytes.
+//     The first tile of every workgroup is located by a search of per-sequence
+//     prefix sums in LDS, computed by each workgroup from the length arrays,
+//     so no host pass or second launch is needed.  A unit cut by a range
 //     boundary is a sequence-wise KV partition whose partial results must be
 //     combined, as the paper notes for its sequence-dimension KV split
 //     (Section 5.2): each piece writes (O/l, lse) to the workspace and counts
@@ -190,12 +195,63 @@ __device__ __forceinline__ int seq_tiles(uint32_t s) {
   return seq_c(s) == 0 ? 0 : (seq_T(s) + C::kTileKeys - 1) / C::kTileKeys;
 }
 
-// Tile schedule shared by every workgroup of a launch: the tiles of all units
-// form one list [0, N), cut into Pe equal contiguous ranges.
+// Cost of one tile of a sequence with c chunk tokens: a fixed part for
+// streaming the tile, plus one per 16-row block of the unit's c * g query
+// rows.  A unit with many rows can take longer on a tile than the tile's
+// HBM stream lasts, so workgroups get equal cost rather than equal tiles.
+constexpr int kTileCost = 6;
+__device__ __forceinline__ int tile_cost(uint32_t s, int g) { return kTileCost + (seq_c(s) * g + kBlk - 1) / kBlk; }
+
+// floor(a / b) for 0 <= a < 2^53 and 0 < b < 2^53: the rounded double
+// quotient is within one of it, and one exact integer step corrects it
+// (much shorter code than a 64-bit integer division).
+__device__ __forceinline__ long long div_floor(long long a, long long b) {
+  long long q = (long long)((double)a / (double)b);
+  const long long r = a - q * b;
+  if (r < 0) --q;
+  else if (r >= b) ++q;
+  return q;
+}
+
+// Tile schedule shared by every workgroup of a launch.  The tiles of all
+// units form one list [0, N) in (sequence, KV head, tile) order; tile t of
+// sequence b starts at cost Hkv cpref[b] + (t - Hkv pref[b]) w_b, w_b its
+// sequence's tile cost, out of Wt in all.  Range q holds the tiles whose start
+// cost lies in [q Wt / Pe, (q + 1) Wt / Pe).  With Pe <= Wt / max_b w_b no
+// range is empty, since consecutive tile starts are at most max_b w_b apart.
 struct Sched {
-  int N, Pe;
-  __device__ int range_begin(int q) const { return (int)((long long)q * N / Pe); }
-  __device__ int owner(int t) const { return (int)(((long long)(t + 1) * Pe - 1) / N); }
+  int N, Pe, B, Hkv, g;
+  bool uni;                 // every tile costs the same: the same ranges, found without a search
+  long long Wt;
+  const uint32_t* seqs;     // packed lengths per sequence
+  const int* pref;          // tiles per KV head of the sequences before b
+  const int* cpref;         // cost of the tiles of one KV head of the sequences before b
+  // range of the tile at offset off = kvh * n + j of sequence b
+  __device__ int owner(int b, int off) const {
+    if (uni) return (int)div_floor((long long)(Hkv * pref[b] + off) * Pe, N);
+    const long long c = (long long)Hkv * cpref[b] + (long long)off * tile_cost(seqs[b], g);
+    return (int)div_floor(c * Pe, Wt);
+  }
+  // first tile of range q (N for q = Pe); every lane of the wave takes part
+  __device__ int range_begin(int q) const {
+    if (q >= Pe) return N;
+    if (uni) return (int)div_floor((long long)q * N + Pe - 1, Pe);
+    const long long X = (long long)q * Wt;
+    // the last sequence b with Hkv cpref[b] Pe <= X: a 64-ary search of the
+    // B + 1 prefix entries; that sequence has tiles, as Hkv cpref[b + 1] Pe > X
+    const int lane = threadIdx.x & 63;
+    const int step = (B + 64) / 64;
+    const int i1 = min(lane * step, B);
+    const long long hp = (long long)Hkv * Pe;
+    const unsigned long long m1 = __ballot(cpref[i1] * hp <= X);
+    const int base = (63 - __builtin_clzll(m1)) * step;
+    const int i2 = min(base + lane, B);
+    const unsigned long long m2 = __ballot(lane < step && cpref[i2] * hp <= X);
+    const int b = __builtin_amdgcn_readfirstlane(base + 63 - __builtin_clzll(m2));
+    const long long den = (long long)tile_cost(seqs[b], g) * Pe;
+    const long long off = div_floor(X - cpref[b] * hp + den - 1, den);   // <= Hkv tiles(b)
+    return Hkv * pref[b] + (int)off;
+  }
 };
 
 // Position of a tile: sequence, KV head, tile index inside the unit, and the
@@ -206,19 +262,17 @@ struct Cursor {
 };
 
 // Merge every piece of a unit; run by the consumer threads of the workgroup
-// whose piece arrived last, after its own tiles.  Range q's piece of the unit
-// is its first segment (slot 2q), except when range q starts before the
-// unit: then it is q's last segment (slot 2q+1).  Each thread takes two
-// (row, 4 d) items per round and issues all their loads before it waits.
+// whose piece arrived last, after its own tiles.  The unit's pieces come from
+// ranges qf..ql; range q's piece is its first segment (slot 2q), except for
+// range qf when it starts before the unit: then it is qf's last segment
+// (slot_first = 2 qf + 1).  Each thread takes two (row, 4 d) items per round
+// and issues all their loads before it waits.
 template <int D>
-__device__ __forceinline__ void merge_unit(const Params& p, const Sched& sc, const uint32_t* seqs, int ctid,
-                                        int unit, int unit_first, int n_unit) {
+__device__ __forceinline__ void merge_unit(const Params& p, const uint32_t* seqs, int ctid, int unit, int qf, int ql,
+                                        int slot_first) {
   const __amdgpu_buffer_rsrc_t ws_o_rsrc = __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
   const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
-  const int qf = sc.owner(unit_first);
-  const int ql = sc.owner(unit_first + n_unit - 1);
-  const int slot_first = 2 * qf + (sc.range_begin(qf) < unit_first ? 1 : 0);
   const int ub = unit / p.Hkv;
   const int ukvh = unit - ub * p.Hkv;
   const int g = p.g;
@@ -291,9 +345,12 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
   __shared__ uint32_t seqs[kMaxSeqs];     // packed (T, c) of every sequence of the launch
   __shared__ int pref[kMaxSeqs + 1];      // tiles per KV head of the sequences before b
-  __shared__ float mst[kConsumers][2][64];   // key-split merge: row max and row sum of each wave
+  __shared__ int cpref[kMaxSeqs + 1];     // cost of one KV head's tiles of the sequences before b
+  __shared__ float mst[kConsumers][2][kBlk];   // key-split merge: max and sum of each wave's rows
   __shared__ int wave_sum[kWaves];
+  __shared__ int wave_cost[kWaves];
   __shared__ int sh_flag[2];              // "this piece completed its unit", for the two pieces
+  __shared__ int sh_share[2][4];          // unit, qf, ql, slot_first of the units of tiles g0 and g1 - 1
   __shared__ int full_cnt[kStages];       // producer waves whose loads of the stage's tile have landed
   __shared__ int empty_cnt[kStages];      // consumer waves done with the stage's tile
   __shared__ int cb_cnt;                  // consumer waves that reached a consumer barrier
@@ -309,48 +366,79 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   const int lg = lane >> 4;               // which quarter of the MFMA k dimension this lane feeds
   const int B = p.B, Hkv = p.Hkv, g = p.g;
 
-  // ---- prologue: lengths and tile prefix sums into LDS (block-wide scan).
-  // Thread tid owns the contiguous sequences [b_lo, b_hi).
+  // ---- prologue: lengths, tile and cost prefix sums into LDS (block-wide
+  // scans).  Thread tid owns the contiguous sequences [b_lo, b_hi).
   const int per = (B + kThreads - 1) / kThreads;
   const int b_lo = min(tid * per, B);
   const int b_hi = min(b_lo + per, B);
-  int my_tiles = 0;
+  int my_tiles = 0, my_cost = 0;   // sums < 2^31 (host check)
   for (int b = b_lo; b < b_hi; ++b) {
     const uint32_t s = load_seq(p, b);
     seqs[b] = s;
     my_tiles += seq_tiles<C>(s);
+    my_cost += seq_tiles<C>(s) * tile_cost(s, g);
   }
-  int incl = my_tiles;
+  int incl = my_tiles, cincl = my_cost;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     const int y = __shfl_up(incl, off);
-    if (lane >= off) incl += y;
+    const int cy = __shfl_up(cincl, off);
+    if (lane >= off) {
+      incl += y;
+      cincl += cy;
+    }
   }
-  if (lane == 63) wave_sum[wave] = incl;
+  if (lane == 63) {
+    wave_sum[wave] = incl;
+    wave_cost[wave] = cincl;
+  }
   if (tid < kStages) {
     full_cnt[tid] = 0;
     empty_cnt[tid] = 0;
   }
   if (tid == 0) cb_cnt = 0;
   __syncthreads();
-  int before = 0, total = 0;
+  int before = 0, total = 0, cbefore = 0, ctotal = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
     before += w < wave ? wave_sum[w] : 0;
     total += wave_sum[w];
+    cbefore += w < wave ? wave_cost[w] : 0;
+    ctotal += wave_cost[w];
   }
   total = uniform(total);
   {
     int run = incl - my_tiles + before;
+    int crun = cincl - my_cost + cbefore;
     for (int b = b_lo; b < b_hi; ++b) {
       pref[b] = run;
+      cpref[b] = crun;
       run += seq_tiles<C>(seqs[b]);
+      crun += seq_tiles<C>(seqs[b]) * tile_cost(seqs[b], g);
     }
-    if (tid == kThreads - 1) pref[B] = total;
+    if (tid == kThreads - 1) {
+      pref[B] = total;
+      cpref[B] = ctotal;
+    }
   }
   Sched sc;
-  sc.N = total * Hkv;           // tiles of all units (< 2^31, host check)
-  sc.Pe = sc.N < p.P ? sc.N : p.P;   // at most one workgroup per tile: no range is empty
+  sc.N = total * Hkv;           // tiles of all units (< 2^30, host check)
+  sc.B = B;
+  sc.Hkv = Hkv;
+  sc.g = g;
+  sc.Wt = (long long)Hkv * ctotal;
+  sc.seqs = seqs;
+  sc.pref = pref;
+  sc.cpref = cpref;
+  {
+    // every tile costs at most w_hi, so with at most Wt / w_hi ranges (and
+    // at least one when there are tiles) no range is empty
+    const int w_hi = kTileCost + (p.C_max * g + kBlk - 1) / kBlk;
+    long long pe = div_floor(sc.Wt, w_hi);
+    if (pe < 1) pe = sc.N > 0 ? 1 : 0;
+    sc.Pe = pe < p.P ? (int)pe : p.P;
+    sc.uni = sc.Wt == (long long)sc.N * w_hi;
+  }
   __syncthreads();
 
   // ---- padding rows c_b <= i < C_max of the sequences b = pid (mod P):
@@ -388,13 +476,6 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     cu.kvh = off / n;
     cu.j = off - cu.kvh * n;
     return cu;
-  };
-  // global index of tile 0 of unit (b, kvh), and the unit's tile count
-  auto unit_tiles = [&](int unit, int& first_tile, int& n) {
-    const int b = unit / Hkv;
-    const int kvh = unit - b * Hkv;
-    n = seq_tiles<C>(uniform(seqs[b]));
-    first_tile = Hkv * uniform(pref[b]) + kvh * n;
   };
 
   // ---- this workgroup's range [g0, g1).  If its last tile lies in a unit
@@ -583,6 +664,27 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       }
     }
     return;
+  }
+  // Only the units of the range's first and last tile can be shared with
+  // other workgroups.  Their piece bookkeeping (the ranges qf..ql that hold
+  // their tiles, and the slot of range qf's piece) is worked out now, while
+  // the first tile streams in, rather than at the end.
+  if (wc == 0) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int t = k == 0 ? g0 : g1 - 1;
+      const Cursor cu = locate(t);
+      const int n = seq_tiles<C>(cu.s);
+      const int qf = sc.owner(cu.b, cu.kvh * n);
+      const int ql = sc.owner(cu.b, cu.kvh * n + n - 1);
+      const int slot_first = 2 * qf + (sc.range_begin(qf) < t - cu.j ? 1 : 0);   // whole wave: a ballot search
+      if (lane == 0) {
+        sh_share[k][0] = cu.b * Hkv + cu.kvh;
+        sh_share[k][1] = qf;
+        sh_share[k][2] = ql;
+        sh_share[k][3] = slot_first;
+      }
+    }
   }
 #pragma unroll
   for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
@@ -831,22 +933,24 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
           f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
 #pragma unroll
           for (int db = 0; db < C::kDB; ++db) reg[db * 64 + lane] = o[db];
-          mst[region][0][lane] = m_run;
-          mst[region][1][lane] = fl;
+          if (lg == 0) {   // the four lanes of a row hold the same values
+            mst[region][0][lm] = m_run;
+            mst[region][1][lm] = fl;
+          }
         }
         cbar();
         if (active) {
           // the same order of operations in every wave of the row block
           float M = -INFINITY;
-          for (int k = 0; k < nks; ++k) M = fmaxf(M, mst[rb * nks + k][0][lane]);
+          for (int k = 0; k < nks; ++k) M = fmaxf(M, mst[rb * nks + k][0][lm]);
           const float Mu = M == -INFINITY ? 0.f : M;
           float wk[kConsumers];
           float L = 0.f;
 #pragma unroll
           for (int k = 0; k < kConsumers; ++k) {
             if (k < nks) {
-              wk[k] = __builtin_amdgcn_exp2f(mst[rb * nks + k][0][lane] - Mu);
-              L += mst[rb * nks + k][1][lane] * wk[k];
+              wk[k] = __builtin_amdgcn_exp2f(mst[rb * nks + k][0][lm] - Mu);
+              L += mst[rb * nks + k][1][lm] * wk[k];
             }
           }
           fm = M;
@@ -898,12 +1002,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 #pragma unroll
     for (int k = 0; k < 2; ++k) {
       const Pub& q = k == 0 ? pub0 : pub1;
-      int flag = 0;
+      int flag = 0;   // 0: no merge here; else 1 + the entry of sh_share for the unit
       if (q.state == 1) {
-        int uf, un;
-        unit_tiles(q.unit, uf, un);
-        const int np = sc.owner(uf + un - 1) - sc.owner(uf) + 1;   // pieces of the unit
-        flag = (k == 0 ? cnt0 : cnt1) + 1 == np ? 1 : 0;
+        const int e = q.unit == sh_share[0][0] ? 0 : 1;
+        const int np = sh_share[e][2] - sh_share[e][1] + 1;   // pieces of the unit
+        flag = (k == 0 ? cnt0 : cnt1) + 1 == np ? 1 + e : 0;
       }
       sh_flag[k] = flag;
     }
@@ -911,11 +1014,10 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   cbar();
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
-    if (sh_flag[k]) {
-      const int unit = k == 0 ? pub0.unit : pub1.unit;
-      int uf, un;
-      unit_tiles(unit, uf, un);
-      merge_unit<D>(p, sc, seqs, ctid, unit, uf, un);
+    const int f = sh_flag[k];
+    if (f) {
+      const int* e = sh_share[f - 1];
+      merge_unit<D>(p, seqs, ctid, e[0], e[1], e[2], e[3]);
     }
   }
 }
@@ -965,6 +1067,9 @@ int validate_desc(const specmoe_verify_desc* d) {
   if (d->S_max >= (1 << 24)) return SPECMOE_ERR_SHAPE;
   const int64_t tile = key_tile(d->dtype, d->D);
   if ((int64_t)kMaxSeqs * d->Hkv * ((d->S_max + tile - 1) / tile) >= ((int64_t)1 << 30)) return SPECMOE_ERR_SHAPE;
+  // the per-KV-head tile cost prefix of the schedule fits in 32 bits
+  const int64_t w_hi = kTileCost + (d->C_max * g + kBlk - 1) / kBlk;
+  if ((int64_t)kMaxSeqs * ((d->S_max + tile - 1) / tile) * w_hi >= ((int64_t)1 << 31)) return SPECMOE_ERR_SHAPE;
   return SPECMOE_OK;
 }
 
