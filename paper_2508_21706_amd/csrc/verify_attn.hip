@@ -168,10 +168,12 @@ __device__ __forceinline__ float row_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Two floats rounded (to nearest even) to bf16 and packed, lo in the low
+// half: one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  __bf16 a = (__bf16)lo;
-  __bf16 b = (__bf16)hi;
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
 }
 
 // Lengths of sequence b, clamped into the documented ranges so that no access
@@ -773,6 +775,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       const int hi = T - (n - 1 - j) * C::kTileKeys;
       const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
       const int nk = hi - lo;
+      const int lim = min(hi - 1, vis);   // this lane's row sees the keys <= lim of the tile
       // Key blocks kb0 and kb1 = kb0 + nks of the tile form a pair: two
       // independent score chains, one softmax step over their 8 keys per
       // lane, and (bf16) one 32-key P V contraction per d block.  A block
@@ -787,25 +790,44 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         // S^T = K Q^T for 16 keys x 16 rows per block; lane (row lm,
         // quarter lg) gets the keys key + 4 lg + r, r = 0..3
         const char* krow = ks + (kb0 * kBlk + lm) * C::kPitch + 16 * lg;
-        f32x4 sa[2];
+        // S^T chunk J of block h: kop(J, h) times Q chunk J
+        auto score = [&](f32x4 acc, const u32x4& kop, int J) {
+          if constexpr (BF16) {
+            return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop),
+                                                           __builtin_bit_cast(bf16x8, qr[J]), acc, 0, 0, 0);
+          } else {
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          u32x4 kop[C::kQJ];
+            for (int e = 0; e < 4; ++e)
+              acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kop[e]), __uint_as_float(qr[J][e]), acc, 0,
+                                                         0, 0);
+            return acc;
+          }
+        };
+        f32x4 sa[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+        if constexpr (C::kQJ <= 4) {
+          // every K operand of the pair is read before the first score MFMA,
+          // in the order the MFMAs take them, so the reads' latency is paid
+          // once and each MFMA waits only for its own operand; the two
+          // chains alternate
+          u32x4 kop[C::kQJ][2];
 #pragma unroll
           for (int J = 0; J < C::kQJ; ++J)
-            kop[J] = *reinterpret_cast<const u32x4*>(krow + h * bstride + 64 * J);
-          sa[h] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int J = 0; J < C::kQJ; ++J) {
-            if constexpr (BF16) {
-              sa[h] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop[J]),
-                                                              __builtin_bit_cast(bf16x8, qr[J]), sa[h], 0, 0, 0);
-            } else {
+            for (int h = 0; h < 2; ++h) kop[J][h] = *reinterpret_cast<const u32x4*>(krow + h * bstride + 64 * J);
+          __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-              for (int e = 0; e < 4; ++e)
-                sa[h] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(kop[J][e]),
-                                                             __uint_as_float(qr[J][e]), sa[h], 0, 0, 0);
-            }
+          for (int J = 0; J < C::kQJ; ++J)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) sa[h] = score(sa[h], kop[J][h], J);
+        } else {
+          // (f32, D = 128: twice the operand registers) one chain at a time
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            u32x4 kop[C::kQJ];
+#pragma unroll
+            for (int J = 0; J < C::kQJ; ++J) kop[J] = *reinterpret_cast<const u32x4*>(krow + h * bstride + 64 * J);
+#pragma unroll
+            for (int J = 0; J < C::kQJ; ++J) sa[h] = score(sa[h], kop[J], J);
           }
         }
 
@@ -830,25 +852,22 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
                   (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + h * bstride + 32 * db));
         }
 
-        // scale, mask, online softmax over the pair's keys
+        // mask, online softmax over the pair's keys (x: unscaled scores)
         float x[8];
         float mx = -INFINITY;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int kbase = h == 0 ? key0 : key1;
-          const bool edge = (kbase + kBlk > hi) || (kbase + kBlk - 1 > l_ctx);
+          // key kbase + 4 lg + r is masked when r > t (past the tile's keys
+          // or past the row's last visible key); never inside the context
+          const int t = lim - (h == 0 ? key0 : key1) - 4 * lg;
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            float xv = sa[h][r] * p.sl2;
-            if (edge) {
-              const int key = kbase + 4 * lg + r;
-              if (key >= hi || key > vis) xv = -INFINITY;
-            }
+            const float xv = r > t ? -INFINITY : sa[h][r];
             x[4 * h + r] = xv;
             mx = fmaxf(mx, xv);
           }
         }
-        mx = row_max(mx);
+        mx = row_max(mx) * p.sl2;   // the scale is positive: max of the scaled scores
         // raise the running max only when the pair's max passes it by
         // more than kLazyMax; the four lanes of a row decide alike
         const bool raise = mx > m_run + kLazyMax;
@@ -864,7 +883,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         float pr[8];
 #pragma unroll
         for (int r = 0; r < 8; ++r) {
-          pr[r] = __builtin_amdgcn_exp2f(x[r] - m_use);
+          pr[r] = __builtin_amdgcn_exp2f(fmaf(x[r], p.sl2, -m_use));
           l_lane += pr[r];
         }
 
