@@ -18,8 +18,9 @@
 //     longer on a tile than the tile takes to stream); when every unit has
 //     the same rows, every workgroup streams the same number of K/V bytes.
 //     The first tile of every workgroup is located by a search of per-sequence
-//     prefix sums in LDS, computed by each workgroup from the length arrays,
-//     so no host pass or second launch is needed.  A unit cut by a range
+//     prefix sums in LDS, computed by one wave of each workgroup from the
+//     length arrays while the others wait at a single barrier, so no host
+//     pass or second launch is needed.  A unit cut by a range
 //     boundary is a sequence-wise KV partition whose partial results must be
 //     combined, as the paper notes for its sequence-dimension KV split
 //     (Section 5.2): each piece writes (O/l, lse) to the workspace and counts
@@ -349,8 +350,6 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   __shared__ int pref[kMaxSeqs + 1];      // tiles per KV head of the sequences before b
   __shared__ int cpref[kMaxSeqs + 1];     // cost of one KV head's tiles of the sequences before b
   __shared__ float mst[kConsumers][2][kBlk];   // key-split merge: max and sum of each wave's rows
-  __shared__ int wave_sum[kWaves];
-  __shared__ int wave_cost[kWaves];
   __shared__ int sh_flag[2];              // "this piece completed its unit", for the two pieces
   __shared__ int sh_share[2][4];          // unit, qf, ql, slot_first of the units of tiles g0 and g1 - 1
   __shared__ int full_cnt[kStages];       // producer waves whose loads of the stage's tile have landed
@@ -368,100 +367,26 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   const int lg = lane >> 4;               // which quarter of the MFMA k dimension this lane feeds
   const int B = p.B, Hkv = p.Hkv, g = p.g;
 
-  // ---- prologue: lengths, tile and cost prefix sums into LDS (block-wide
-  // scans).  Thread tid owns the contiguous sequences [b_lo, b_hi).
-  const int per = (B + kThreads - 1) / kThreads;
-  const int b_lo = min(tid * per, B);
-  const int b_hi = min(b_lo + per, B);
-  int my_tiles = 0, my_cost = 0;   // sums < 2^31 (host check)
-  for (int b = b_lo; b < b_hi; ++b) {
-    const uint32_t s = load_seq(p, b);
-    seqs[b] = s;
-    my_tiles += seq_tiles<C>(s);
-    my_cost += seq_tiles<C>(s) * tile_cost(s, g);
-  }
-  int incl = my_tiles, cincl = my_cost;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(incl, off);
-    const int cy = __shfl_up(cincl, off);
-    if (lane >= off) {
-      incl += y;
-      cincl += cy;
-    }
-  }
-  if (lane == 63) {
-    wave_sum[wave] = incl;
-    wave_cost[wave] = cincl;
-  }
-  if (tid < kStages) {
-    full_cnt[tid] = 0;
-    empty_cnt[tid] = 0;
-  }
-  if (tid == 0) cb_cnt = 0;
-  __syncthreads();
-  int before = 0, total = 0, cbefore = 0, ctotal = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    before += w < wave ? wave_sum[w] : 0;
-    total += wave_sum[w];
-    cbefore += w < wave ? wave_cost[w] : 0;
-    ctotal += wave_cost[w];
-  }
-  total = uniform(total);
-  {
-    int run = incl - my_tiles + before;
-    int crun = cincl - my_cost + cbefore;
-    for (int b = b_lo; b < b_hi; ++b) {
-      pref[b] = run;
-      cpref[b] = crun;
-      run += seq_tiles<C>(seqs[b]);
-      crun += seq_tiles<C>(seqs[b]) * tile_cost(seqs[b], g);
-    }
-    if (tid == kThreads - 1) {
-      pref[B] = total;
-      cpref[B] = ctotal;
-    }
-  }
-  Sched sc;
-  sc.N = total * Hkv;           // tiles of all units (< 2^30, host check)
-  sc.B = B;
-  sc.Hkv = Hkv;
-  sc.g = g;
-  sc.Wt = (long long)Hkv * ctotal;
-  sc.seqs = seqs;
-  sc.pref = pref;
-  sc.cpref = cpref;
-  {
-    // every tile costs at most w_hi, so with at most Wt / w_hi ranges (and
-    // at least one when there are tiles) no range is empty
-    const int w_hi = kTileCost + (p.C_max * g + kBlk - 1) / kBlk;
-    long long pe = div_floor(sc.Wt, w_hi);
-    if (pe < 1) pe = sc.N > 0 ? 1 : 0;
-    sc.Pe = pe < p.P ? (int)pe : p.P;
-    sc.uni = sc.Wt == (long long)sc.N * w_hi;
-  }
-  __syncthreads();
-
   // ---- padding rows c_b <= i < C_max of the sequences b = pid (mod P):
-  // out = 0, lse = -inf.
-  for (int b = pid; b < B; b += p.P) {
-    const int c = seq_c(seqs[b]);
-    const int pad_rows = (p.C_max - c) * p.Hq;
-    for (int idx = tid; idx < pad_rows * (D / 4); idx += kThreads) {
-      const int r = idx / (D / 4);
-      const int d4 = idx - r * (D / 4);
-      const int i = c + r / p.Hq;
-      const int h = r % p.Hq;
-      const size_t orow = (size_t)(b * p.C_max + i) * p.Hq + h;
-      *reinterpret_cast<f32x4*>(p.out + orow * D + 4 * d4) = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (d4 == 0) p.lse[orow] = -INFINITY;
+  // out = 0, lse = -inf; written by threads t0, t0 + stride, ...
+  auto pad_rows = [&](int t0, int stride) {
+    for (int b = pid; b < B; b += p.P) {
+      const int c = seq_c(seqs[b]);
+      const int pad_rows_b = (p.C_max - c) * p.Hq;
+      for (int idx = t0; idx < pad_rows_b * (D / 4); idx += stride) {
+        const int r = idx / (D / 4);
+        const int d4 = idx - r * (D / 4);
+        const int i = c + r / p.Hq;
+        const int h = r % p.Hq;
+        const size_t orow = (size_t)(b * p.C_max + i) * p.Hq + h;
+        *reinterpret_cast<f32x4*>(p.out + orow * D + 4 * d4) = f32x4{0.f, 0.f, 0.f, 0.f};
+        if (d4 == 0) p.lse[orow] = -INFINITY;
+      }
     }
-  }
-  if (pid >= sc.Pe) return;
+  };
 
-  // Cursor of global tile t: a 64-ary search of the prefix sums, done by
-  // every wave on its own (two LDS reads and two ballots).
+  // Cursor of global tile t: a 64-ary search of the prefix sums, done by a
+  // whole wave (two LDS reads and two ballots).
   auto locate = [&](int t) {
     const int tq = t / Hkv;                      // tiles per KV head before t's sequence, at most
     const int step = (B + 64) / 64;              // B + 1 prefix entries in 64 groups
@@ -479,19 +404,120 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     cu.j = off - cu.kvh * n;
     return cu;
   };
+  Sched sc;
+  sc.B = B;
+  sc.Hkv = Hkv;
+  sc.g = g;
+  sc.seqs = seqs;
+  sc.pref = pref;
+  sc.cpref = cpref;
+  // every tile costs at most w_hi, so with at most Wt / w_hi ranges (and at
+  // least one when there are tiles) no range is empty
+  const int w_hi = kTileCost + (p.C_max * g + kBlk - 1) / kBlk;
+  auto set_totals = [&](int tiles_per_head, int cost_per_head) {
+    sc.N = tiles_per_head * Hkv;   // tiles of all units (< 2^30, host check)
+    sc.Wt = (long long)Hkv * cost_per_head;
+    long long pe = div_floor(sc.Wt, w_hi);
+    if (pe < 1) pe = sc.N > 0 ? 1 : 0;
+    sc.Pe = pe < p.P ? (int)pe : p.P;
+    sc.uni = sc.Wt == (long long)sc.N * w_hi;
+  };
 
-  // ---- this workgroup's range [g0, g1).  If its last tile lies in a unit
-  // that starts inside the range and continues past it, that last segment
-  // [s_last, g1) is streamed first, then [g0, s_last).
-  const int g0 = sc.range_begin(pid);
-  const int g1 = sc.range_begin(pid + 1);
+  // ---- prologue, by wave 0 alone while the other waves wait at one
+  // barrier (every wave doing it was issue-bound): the lengths, tile and cost
+  // prefix sums into LDS, then this workgroup's range [g0, g1) and its first
+  // tile.  Lane l owns the contiguous sequences [l per, (l + 1) per).  If the
+  // range's last tile lies in a unit that starts inside the range and
+  // continues past it, that last segment [s_last, g1) is streamed first,
+  // then [g0, s_last).
+  __shared__ int sh_sched[12];
+  if (wave == 0) {
+    const int per = (B + 63) / 64;
+    const int b_lo = min(lane * per, B);
+    const int b_hi = min(b_lo + per, B);
+    int my_tiles = 0, my_cost = 0;   // sums < 2^31 (host check)
+    for (int b = b_lo; b < b_hi; ++b) {
+      const uint32_t s = load_seq(p, b);
+      seqs[b] = s;
+      my_tiles += seq_tiles<C>(s);
+      my_cost += seq_tiles<C>(s) * tile_cost(s, g);
+    }
+    int incl = my_tiles, cincl = my_cost;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(incl, off);
+      const int cy = __shfl_up(cincl, off);
+      if (lane >= off) {
+        incl += y;
+        cincl += cy;
+      }
+    }
+    const int total = __builtin_amdgcn_readlane(incl, 63);
+    const int ctotal = __builtin_amdgcn_readlane(cincl, 63);
+    int run = incl - my_tiles, crun = cincl - my_cost;
+    for (int b = b_lo; b < b_hi; ++b) {
+      pref[b] = run;
+      cpref[b] = crun;
+      run += seq_tiles<C>(seqs[b]);
+      crun += seq_tiles<C>(seqs[b]) * tile_cost(seqs[b], g);
+    }
+    if (lane == 63) {
+      pref[B] = total;
+      cpref[B] = ctotal;
+    }
+    if (lane < kStages) {
+      full_cnt[lane] = 0;
+      empty_cnt[lane] = 0;
+    }
+    if (lane == 0) cb_cnt = 0;
+    set_totals(total, ctotal);
+    int g0 = 0, g1 = 0, nL = 0, s_last = 0;
+    Cursor first = {0, 0, 0, 0u};
+    if (pid < sc.Pe) {
+      g0 = sc.range_begin(pid);
+      g1 = sc.range_begin(pid + 1);
+      first = locate(g1 - 1);
+      s_last = g1 - 1 - first.j;
+      const bool rotated = s_last > g0 && first.j < seq_tiles<C>(first.s) - 1;
+      nL = rotated ? g1 - s_last : 0;    // tiles of the rotated segment
+      if (rotated) first.j = 0;
+      else first = locate(g0);
+    }
+    if (lane == 0) {
+      sh_sched[0] = total;
+      sh_sched[1] = ctotal;
+      sh_sched[9] = sc.Pe;
+      sh_sched[10] = sc.uni ? 1 : 0;
+      sh_sched[2] = g0;
+      sh_sched[3] = g1;
+      sh_sched[4] = nL;
+      sh_sched[5] = s_last;
+      sh_sched[6] = first.b;
+      sh_sched[7] = first.kvh;
+      sh_sched[8] = first.j;
+    }
+  }
+  __syncthreads();
+  if (wave != 0) {
+    sc.N = uniform(sh_sched[0]) * Hkv;
+    sc.Wt = (long long)Hkv * uniform(sh_sched[1]);
+    sc.Pe = uniform(sh_sched[9]);
+    sc.uni = uniform(sh_sched[10]) != 0;
+  }
+  if (pid >= sc.Pe) {
+    pad_rows(tid, kThreads);
+    return;
+  }
+  const int g0 = uniform(sh_sched[2]);
+  const int g1 = uniform(sh_sched[3]);
+  const int nL = uniform(sh_sched[4]);
+  const int s_last = uniform(sh_sched[5]);
   const int count = g1 - g0;
-  Cursor first = locate(g1 - 1);
-  const int s_last = g1 - 1 - first.j;
-  const bool rotated = s_last > g0 && first.j < seq_tiles<C>(first.s) - 1;
-  const int nL = rotated ? g1 - s_last : 0;    // tiles of the rotated segment
-  if (rotated) first.j = 0;
-  else first = locate(g0);
+  Cursor first;
+  first.b = uniform(sh_sched[6]);
+  first.kvh = uniform(sh_sched[7]);
+  first.j = uniform(sh_sched[8]);
+  first.s = uniform(seqs[first.b]);
   // global index of the tile at position v of the workgroup's order
   auto tile_at = [&](int v) { return v < nL ? s_last + v : g0 + (v - nL); };
   // the first tile of unit (b, kvh) after cursor cu's unit
@@ -637,26 +663,26 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     wait_count(&cb_cnt, kConsumers * ncb);
   };
 
-  // The first unit's Q goes out before any tile load, so that it does not
-  // queue behind the tiles: consumers issue it, then every wave meets at a
-  // barrier (one that does not wait for those loads), then the producers
-  // start.  It arrives through qn, so that qr is only ever written from
-  // registers and the score MFMAs never wait for a load.
+  // The first unit's Q arrives through qn, so that qr is only ever written
+  // from registers and the score MFMAs never wait for a load.  The producers
+  // start at once: the Q loads need not go out before the first tile's.
   if (!producer) load_q(first, qn);
-  asm volatile("s_barrier" ::: "memory");
   if (producer) {
     // Producer pair grp streams the tiles v = grp, grp + 2, ... of the
     // workgroup's order into stage grp: it waits until all consumers have
     // released the stage's previous tile, issues the loads, waits for its own
     // loads to land and counts itself on the stage's fill counter.  The two
     // pairs run independently, so one tile's loads are issued while the
-    // other's are still in flight.
+    // other's are still in flight; only tile 1 waits until tile 0 has landed,
+    // so that at the start, when every workgroup asks for its first tiles at
+    // once, tile 0 is not delivered interleaved with tile 1.
     const int grp = wave >> 1;
     Cursor cu = first;
     int v = grp;
     if (grp == 1 && count > 1) advance(cu, 0);
     for (; v < count; v += 2) {
       if (v >= 2) wait_count(&empty_cnt[grp], kConsumers * (v >> 1));
+      if (v == 1) wait_count(&full_cnt[0], 2);
       dma(cu, grp);
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       signal_count(&full_cnt[grp]);
@@ -697,6 +723,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const Cursor c1 = next_segment(first, 0, v1);
     if (v1 < count) load_q(c1, qn);   // the second segment's Q
   }
+  pad_rows(ctid, kCThreads);   // while the first tile streams in
   Cursor cur = first;                  // cursor of the tile being computed
   int seg_g = g0;
   // results of the segment that ended in the previous iteration, stored at
