@@ -264,59 +264,85 @@ struct Cursor {
   uint32_t s;
 };
 
-// Merge every piece of a unit; run by the consumer threads of the workgroup
-// whose piece arrived last, after its own tiles.  The unit's pieces come from
-// ranges qf..ql; range q's piece is its first segment (slot 2q), except for
-// range qf when it starts before the unit: then it is qf's last segment
-// (slot_first = 2 qf + 1).  Each thread takes two (row, 4 d) items per round
-// and issues all their loads before it waits.
+// Merge every piece of up to two units: those whose last piece this
+// workgroup published, run by its consumer threads after its own tiles.  A
+// unit's pieces come from ranges qf..ql; range q's piece is its first
+// segment (slot 2q), except for range qf when it starts before the unit:
+// then it is qf's last segment (slot_first = 2 qf + 1).  The (row, 4 d)
+// items of both units form one list, and each thread takes three items per
+// round and issues all their loads before it waits, so the two units' loads
+// go out together.  Unit u is described by e_u = {unit, qf, ql, slot_first}.
 template <int D>
-__device__ __forceinline__ void merge_unit(const Params& p, const uint32_t* seqs, int ctid, int unit, int qf, int ql,
-                                        int slot_first) {
+__device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seqs, int ctid, const int* e_a,
+                                         const int* e_b, bool has_a, bool has_b) {
   const __amdgpu_buffer_rsrc_t ws_o_rsrc = __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
   const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
-  const int ub = unit / p.Hkv;
-  const int ukvh = unit - ub * p.Hkv;
   const int g = p.g;
-  const int n_items = seq_c(uniform(seqs[ub])) * g * (D / 4);
+  int ua = 0, qfa = 0, qla = -1, sfa = 0, ub = 0, qfb = 0, qlb = -1, sfb = 0;
+  if (has_a) {
+    ua = uniform(e_a[0]);
+    qfa = uniform(e_a[1]);
+    qla = uniform(e_a[2]);
+    sfa = uniform(e_a[3]);
+  }
+  if (has_b) {
+    ub = uniform(e_b[0]);
+    qfb = uniform(e_b[1]);
+    qlb = uniform(e_b[2]);
+    sfb = uniform(e_b[3]);
+  }
+  const int n_a = has_a ? seq_c(uniform(seqs[ua / p.Hkv])) * g * (D / 4) : 0;
+  const int n_b = has_b ? seq_c(uniform(seqs[ub / p.Hkv])) * g * (D / 4) : 0;
+  const int n_items = n_a + n_b;
+  const int np_max = max(qla - qfa, qlb - qfb) + 1;   // pieces of the larger unit
   constexpr int kBatch = 4;   // pieces loaded per item before combining
-  constexpr int kItems = 2;   // items per thread and round
+  constexpr int kItems = 3;   // items per thread and round
   for (int base = ctid; base < n_items; base += kItems * kCThreads) {
     float m[kItems], z[kItems];
     f32x4 acc[kItems];
+    int srow0[kItems], qf[kItems], ql[kItems], sf[kItems], d0[kItems];
+    size_t orow[kItems];
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
       m[it] = -INFINITY;
       z[it] = 0.f;
       acc[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int idx = base + it * kCThreads;
+      const bool in_a = idx < n_a;
+      const int unit = in_a ? ua : ub;
+      const int local = in_a ? idx : idx - n_a;
+      const int r = local / (D / 4);
+      d0[it] = 4 * (local - r * (D / 4));
+      qf[it] = in_a ? qfa : qfb;
+      ql[it] = idx < n_items ? (in_a ? qla : qlb) : -1;   // no pieces for a lane past the items
+      sf[it] = in_a ? sfa : sfb;
+      srow0[it] = r;
+      const int b = unit / p.Hkv;
+      orow[it] = (size_t)(b * p.C_max + r / g) * p.Hq + (unit - b * p.Hkv) * g + r % g;
     }
-    for (int q0 = qf; q0 <= ql; q0 += kBatch) {
+    for (int k0 = 0; k0 < np_max; k0 += kBatch) {
       float lq[kItems][kBatch];
       f32x4 x[kItems][kBatch];
 #pragma unroll
       for (int it = 0; it < kItems; ++it) {
-        const int idx = base + it * kCThreads;
-        const int r = idx / (D / 4);
-        const int d0 = 4 * (idx - r * (D / 4));
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-          const int q = q0 + u;
-          const int srow = (q == qf ? slot_first : 2 * q) * p.Rcap + r;
-          if (idx < n_items && q <= ql) {
+          const int q = qf[it] + k0 + u;
+          const int srow = (k0 + u == 0 ? sf[it] : 2 * q) * p.Rcap + srow0[it];
+          if (q <= ql[it]) {
             lq[it][u] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ws_lse_rsrc, srow * 4, 0,
                                                                                      kDeviceCoherent));
             x[it][u] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                     ws_o_rsrc, (srow * D + d0) * 4, 0, kDeviceCoherent));
+                                                     ws_o_rsrc, (srow * D + d0[it]) * 4, 0, kDeviceCoherent));
           }
         }
       }
 #pragma unroll
       for (int it = 0; it < kItems; ++it) {
-        if (base + it * kCThreads >= n_items) continue;
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-          if (q0 + u > ql) break;
+          if (qf[it] + k0 + u > ql[it]) break;
           if (lq[it][u] == -INFINITY) continue;   // a piece in which this row sees no key
           const float nm = fmaxf(m[it], lq[it][u]);
           const float a = expf(m[it] - nm);
@@ -329,17 +355,15 @@ __device__ __forceinline__ void merge_unit(const Params& p, const uint32_t* seqs
     }
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
-      const int idx = base + it * kCThreads;
-      if (idx >= n_items) continue;
-      const int r = idx / (D / 4);
-      const int d0 = 4 * (idx - r * (D / 4));
-      const size_t orow = (size_t)(ub * p.C_max + r / g) * p.Hq + ukvh * g + r % g;
-      *reinterpret_cast<f32x4*>(p.out + orow * D + d0) = acc[it] * (1.f / z[it]);
-      if (d0 == 0) p.lse[orow] = m[it] + logf(z[it]);
+      if (base + it * kCThreads >= n_items) continue;
+      *reinterpret_cast<f32x4*>(p.out + orow[it] * D + d0[it]) = acc[it] * (1.f / z[it]);
+      if (d0[it] == 0) p.lse[orow[it]] = m[it] + logf(z[it]);
     }
   }
-  if (ctid == 0)   // ready for the next call
-    __hip_atomic_store(p.counters + unit, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (ctid == 0) {   // ready for the next call
+    if (has_a) __hip_atomic_store(p.counters + ua, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (has_b) __hip_atomic_store(p.counters + ub, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
 }
 
 template <bool BF16, int D>
@@ -1058,13 +1082,9 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     }
   }
   cbar();
-#pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int f = sh_flag[k];
-    if (f) {
-      const int* e = sh_share[f - 1];
-      merge_unit<D>(p, seqs, ctid, e[0], e[1], e[2], e[3]);
-    }
+  {
+    const int f0 = sh_flag[0], f1 = sh_flag[1];
+    if (f0 || f1) merge_units<D>(p, seqs, ctid, sh_share[f0 ? f0 - 1 : 0], sh_share[f1 ? f1 - 1 : 0], f0 != 0, f1 != 0);
   }
 }
 
