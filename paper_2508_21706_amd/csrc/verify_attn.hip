@@ -613,11 +613,13 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 
 
   // ---- consumer roles for the unit of cursor cu.  Rows are cut into
-  // n_rb 16-row blocks (n_rbp = n_rb rounded up to a power of two); consumer
-  // wave wc takes row block rb = wc % n_rbp, and the nks waves of a row block
-  // share every tile's key blocks: wave kslot takes the pairs
-  // (kb, kb + nks) for kb = kslot, kslot + 2 nks, ...  (nks <= kNKB / 2, so
-  // every wave has whole pairs).
+  // n_rb 16-row blocks; consumer wave wc takes row block rb = wc % n_rbp, and
+  // the nks = 8 / n_rbp waves of a row block share every tile's key blocks:
+  // wave kslot takes the pairs (kb, kb + nks) for kb = kslot, kslot + 2 nks,
+  // ...  (nks <= kNKB / 2, so every wave has whole pairs).  n_rbp is 1 or 2
+  // for one or two row blocks (four waves per block), else 8: from three
+  // blocks on, a wave computes its block's whole tile, which is cheaper than
+  // merging the waves' partial states at the end of every unit.
   int R = 0, n_rbp = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
   bool active = false, row_valid = false;
   auto roles = [&](const Cursor& cu) {
@@ -625,7 +627,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     R = c * g;
     l_ctx = seq_T(cu.s) - c;
     const int n_rb = (R + kBlk - 1) / kBlk;
-    n_rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : n_rb <= 4 ? 4 : 8;
+    n_rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : 8;
     nks = min(kConsumers / n_rbp, C::kNKB / 2);   // consumers that share a row block
     rb = producer ? 0 : wc % n_rbp;
     kslot = producer ? nks : wc / n_rbp;
@@ -641,7 +643,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int c = seq_c(cu.s);
     const int uR = c * g;
     const int n_rb = (uR + kBlk - 1) / kBlk;
-    const int rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : n_rb <= 4 ? 4 : 8;
+    const int rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : 8;
     const int rb_ = wc % rbp;
     const int ks_ = wc / rbp;
     const int row_ = rb_ * kBlk + lm;

@@ -171,6 +171,9 @@ EDGE = {
     "tile_boundaries": (6, 8, 2, 128, "bf16", [123, 127, 128, 129, 255, 507], [5, 1, 2, 5, 1, 5], 5),
     "three_row_tiles": (4, 28, 4, 128, "bf16", [700, 33, 1500, 2], [10, 12, 13, 16], 16),
     "max_rows_128": (2, 32, 4, 128, "bf16", [900, 64], [16, 16], 16),
+    # 3 and 4 row blocks per unit: one wave per block, no key split
+    "rows_three_four_blocks": (4, 32, 4, 128, "bf16", [300, 1000, 77, 129], [5, 8, 6, 7], 8),
+    "f32_d64_three_blocks": (2, 16, 2, 64, "f32", [200, 150], [5, 6], 6),
     "mha_g1": (3, 8, 8, 128, "bf16", [400, 10, 1000], [4, 2, 3], 4),
     "bf16_d64": (3, 16, 4, 64, "bf16", [500, 260, 1], [5, 3, 5], 5),
     "f32_d128": (2, 8, 2, 128, "f32", [300, 77], [4, 2], 4),
