@@ -169,6 +169,19 @@ __device__ __forceinline__ float row_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave (all active): shifts
+// within each 16-lane row, then row 0's and row 1's last lanes broadcast into
+// the rows after them.  DPP moves, no LDS round trip.
+__device__ __forceinline__ int wave_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, false);   // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15 into rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
 // Two floats rounded (to nearest even) to bf16 and packed, lo in the low
 // half: one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
@@ -466,16 +479,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       my_tiles += seq_tiles<C>(s);
       my_cost += seq_tiles<C>(s) * tile_cost(s, g);
     }
-    int incl = my_tiles, cincl = my_cost;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int y = __shfl_up(incl, off);
-      const int cy = __shfl_up(cincl, off);
-      if (lane >= off) {
-        incl += y;
-        cincl += cy;
-      }
-    }
+    const int incl = wave_scan(my_tiles), cincl = wave_scan(my_cost);
     const int total = __builtin_amdgcn_readlane(incl, 63);
     const int ctotal = __builtin_amdgcn_readlane(cincl, 63);
     int run = incl - my_tiles, crun = cincl - my_cost;
