@@ -44,6 +44,12 @@ def build(verbose: bool = False, output: str = OUTPUT) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
+    # every symbol must resolve: a kernel template whose host-side stub the
+    # compiler silently failed to emit links fine but cannot be loaded
+    check = subprocess.run([sys.executable, "-c", f"import ctypes; ctypes.CDLL({tmp!r})"],
+                           capture_output=True, text=True)
+    if check.returncode != 0:
+        raise RuntimeError(f"built library does not load:\n{check.stderr.strip().splitlines()[-1]}")
     os.replace(tmp, output)
     return output
 

@@ -35,8 +35,9 @@
 //     handed over through LDS counters (no workgroup barrier on the tile
 //     path), so one pair's tile is in flight while the other's is computed.
 //     Only the producers issue tile loads, so a consumer's wait for its own
-//     stores or loads never drains the tile stream.  LDS rows are padded by
-//     16 bytes, so every MFMA operand read is free of bank conflicts and all
+//     stores or loads never drains the tile stream.  Staged K rows are padded
+//     by 16 bytes and (bf16, D = 128) V rows by 32, so the score operand
+//     reads and the transposed V reads are free of bank conflicts, and all
 //     operand addresses are a per-lane base plus an immediate.
 //   * Scores are formed transposed, S^T = K Q^T (keys on the MFMA M side,
 //     query rows on N), so each lane holds one query row and four keys: row
@@ -116,15 +117,24 @@ struct Cfg {
   static constexpr int kRowBytes = D * kElt;
   static constexpr int kChunks = kRowBytes / 16;           // 16-byte chunks per row
   static constexpr int kTileKeys = kHalf / kRowBytes;
-  static constexpr int kSlots = kChunks + 1;                // LDS slots per row: the chunks and one pad
-  static constexpr int kPitch = 16 * kSlots;                // padded LDS row pitch
-  static constexpr int kLdsHalf = kTileKeys * kPitch;       // LDS bytes of a staged K (or V) tile
-  static constexpr int kStage = 2 * kLdsHalf;
-  static constexpr int kInst = (kTileKeys * kSlots + 63) / 64;   // 64-slot DMA instructions per K (or V) tile
+  // LDS slots per staged row: the chunks and pad slots.  K rows carry one
+  // pad (a 16-byte shift per row: the 16 rows of a score operand read sit in
+  // distinct banks).  bf16 D = 128 V rows carry two (a 32-byte shift: the
+  // transposed V reads take 4 rows x 32 bytes per 16 lanes, which one pad
+  // would leave two-way bank conflicted); other layouts keep one.
+  static constexpr int kSlotsK = kChunks + 1;
+  static constexpr int kSlotsV = kChunks + (BF16 && D == 128 ? 2 : 1);
+  static constexpr int kPitchK = 16 * kSlotsK;              // padded LDS row pitches
+  static constexpr int kPitchV = 16 * kSlotsV;
+  static constexpr int kLdsK = kTileKeys * kPitchK;         // LDS bytes of a staged K (V) tile
+  static constexpr int kLdsV = kTileKeys * kPitchV;
+  static constexpr int kStage = kLdsK + kLdsV;
+  static constexpr int kInstK = (kTileKeys * kSlotsK + 63) / 64;   // 64-slot DMA instructions per K (V) tile
+  static constexpr int kInstV = (kTileKeys * kSlotsV + 63) / 64;
   static constexpr int kNKB = kTileKeys / kBlk;             // 16-key blocks per tile
   static constexpr int kDB = D / 16;                        // 16-wide d blocks of O^T
   static constexpr int kQJ = kChunks / 4;                   // 16-byte Q chunks per lane
-  static_assert(kInst <= 2 * kMaxDma, "DMA instructions per producer wave");
+  static_assert(kInstK <= 2 * kMaxDma && kInstV <= 2 * kMaxDma, "DMA instructions per producer wave");
   static_assert(kStages * kStage + 12 * 1024 + 256 <= 160 * 1024, "LDS budget");
   static_assert(kConsumers * 64 * D <= kStage, "key-split merge scratch fits in a stage");
   static_assert(kNKB >= 2, "key blocks are processed in pairs");
@@ -596,22 +606,27 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const char* kp = p.k + slab + (size_t)lo * C::kRowBytes;
     const char* vp = p.v + slab + (size_t)lo * C::kRowBytes;
     char* kl = smem + st * C::kStage;
-    char* vl = kl + C::kLdsHalf;
+    char* vl = kl + C::kLdsK;
 #pragma unroll
     for (int k = 0; k < kMaxDma; ++k) {
       const int i = pw + 2 * k;
       const int sl = 64 * i + lane;
-      if (i < C::kInst && sl < C::kTileKeys * C::kSlots) {
-        const int drow = sl / C::kSlots;
-        const int dch = min(sl - drow * C::kSlots, C::kChunks - 1);
-        const uint32_t off = (uint32_t)min(drow, last) * C::kRowBytes + 16u * dch;
-        // a K load whose first row is past the tile's keys is skipped: those
-        // scores are masked whatever the slots hold
-        if ((64 * i) / C::kSlots <= last)
-          __builtin_amdgcn_global_load_lds(kp + off, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
-                                           0);
-        __builtin_amdgcn_global_load_lds(vp + off, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0, 0);
-      }
+      // source offset of LDS slot sl in each half (a pad slot re-reads its
+      // row's last chunk)
+      const int krow_ = sl / C::kSlotsK;
+      const uint32_t koff =
+          (uint32_t)min(krow_, last) * C::kRowBytes + 16u * min(sl - krow_ * C::kSlotsK, C::kChunks - 1);
+      const int vrow_ = sl / C::kSlotsV;
+      const uint32_t voff =
+          (uint32_t)min(vrow_, last) * C::kRowBytes + 16u * min(sl - vrow_ * C::kSlotsV, C::kChunks - 1);
+      // a K load whose first row is past the tile's keys is skipped: those
+      // scores are masked whatever the slots hold
+      if (i < C::kInstK && sl < C::kTileKeys * C::kSlotsK && (64 * i) / C::kSlotsK <= last)
+        __builtin_amdgcn_global_load_lds(kp + koff, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
+                                         0);
+      if (i < C::kInstV && sl < C::kTileKeys * C::kSlotsV)
+        __builtin_amdgcn_global_load_lds(vp + voff, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0,
+                                         0);
     }
   };
 
@@ -626,19 +641,25 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // merging the waves' partial states at the end of every unit.
   int R = 0, n_rbp = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
   bool active = false, row_valid = false;
+  // x / g for a row 0 <= x < 128 of a unit, by a float reciprocal: exact
+  // there, as (x + 1/2) / g lies at least 1 / (2 g) from an integer
+  const float inv_g = 1.f / (float)g;
+  auto div_g = [&](int x) { return (int)(((float)x + 0.5f) * inv_g); };
+  auto rbp_shift = [&](int n_rb) { return n_rb <= 1 ? 0 : n_rb <= 2 ? 1 : 3; };   // log2 n_rbp
   auto roles = [&](const Cursor& cu) {
     const int c = seq_c(cu.s);
     R = c * g;
     l_ctx = seq_T(cu.s) - c;
     const int n_rb = (R + kBlk - 1) / kBlk;
-    n_rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : 8;
-    nks = min(kConsumers / n_rbp, C::kNKB / 2);   // consumers that share a row block
-    rb = producer ? 0 : wc % n_rbp;
-    kslot = producer ? nks : wc / n_rbp;
+    const int sh = rbp_shift(n_rb);
+    n_rbp = 1 << sh;
+    nks = min(kConsumers >> sh, C::kNKB / 2);   // consumers that share a row block
+    rb = producer ? 0 : wc & (n_rbp - 1);
+    kslot = producer ? nks : wc >> sh;
     active = !producer && rb < n_rb && kslot < nks;
     row = rb * kBlk + lm;
     row_valid = active && row < R;
-    tok = row_valid ? row / g : 0;
+    tok = row_valid ? div_g(row) : 0;
     vis = row_valid ? l_ctx + tok : 0x7fffffff;   // last visible key of this lane's row
   };
   // Q chunks of this lane's row for the unit of cu (zero for invalid rows):
@@ -647,14 +668,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int c = seq_c(cu.s);
     const int uR = c * g;
     const int n_rb = (uR + kBlk - 1) / kBlk;
-    const int rbp = n_rb <= 1 ? 1 : n_rb <= 2 ? 2 : 8;
-    const int rb_ = wc % rbp;
-    const int ks_ = wc / rbp;
+    const int sh = rbp_shift(n_rb);
+    const int rb_ = wc & ((1 << sh) - 1);
+    const int ks_ = wc >> sh;
     const int row_ = rb_ * kBlk + lm;
-    const bool ok = rb_ < n_rb && ks_ < min(kConsumers / rbp, C::kNKB / 2) && row_ < uR;
-    const int tk = ok ? row_ / g : 0;
+    const bool ok = rb_ < n_rb && ks_ < min(kConsumers >> sh, C::kNKB / 2) && row_ < uR;
+    const int tk = ok ? div_g(row_) : 0;
     const char* qrow =
-        p.q + ((size_t)(cu.b * p.C_max + tk) * p.Hq + cu.kvh * g + (ok ? row_ % g : 0)) * C::kRowBytes;
+        p.q + ((size_t)(cu.b * p.C_max + tk) * p.Hq + cu.kvh * g + (ok ? row_ - tk * g : 0)) * C::kRowBytes;
 #pragma unroll
     for (int J = 0; J < C::kQJ; ++J)
       dst[J] = ok ? *reinterpret_cast<const u32x4*>(qrow + 16 * (4 * J + lg)) : u32x4{0u, 0u, 0u, 0u};
@@ -827,7 +848,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 
     {
       const char* ks = smem + st * C::kStage;
-      const char* vs = ks + C::kLdsHalf;
+      const char* vs = ks + C::kLdsK;
       const int T = seq_T(s);
       const int hi = T - (n - 1 - j) * C::kTileKeys;
       const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
@@ -843,10 +864,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         if (kb0 * kBlk >= nk) break;
         const int key0 = lo + kb0 * kBlk;
         const int key1 = key0 + nks * kBlk;
-        const int bstride = nks * kBlk * C::kPitch;   // LDS bytes from block kb0 to kb1
+        const int bstride = nks * kBlk * C::kPitchK;    // LDS bytes from block kb0 to kb1 (K)
+        const int vbstride = nks * kBlk * C::kPitchV;   // (V)
         // S^T = K Q^T for 16 keys x 16 rows per block; lane (row lm,
         // quarter lg) gets the keys key + 4 lg + r, r = 0..3
-        const char* krow = ks + (kb0 * kBlk + lm) * C::kPitch + 16 * lg;
+        const char* krow = ks + (kb0 * kBlk + lm) * C::kPitchK + 16 * lg;
         // S^T chunk J of block h: kop(J, h) times Q chunk J
         auto score = [&](f32x4 acc, const u32x4& kop, int J) {
           if constexpr (BF16) {
@@ -900,13 +922,13 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         i16x4 vt[BF16 ? 2 * C::kDB : 1];
         if constexpr (BF16) {
           typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-          const char* vrow = vs + (kb0 * kBlk + 4 * lg + (lm >> 2)) * C::kPitch + 8 * (lm & 3);
+          const char* vrow = vs + (kb0 * kBlk + 4 * lg + (lm >> 2)) * C::kPitchV + 8 * (lm & 3);
 #pragma unroll
           for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int db = 0; db < C::kDB; ++db)
               vt[h * C::kDB + db] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                  (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + h * bstride + 32 * db));
+                  (lds_i16x4*)(__attribute__((address_space(3))) char*)(vrow + h * vbstride + 32 * db));
         }
 
         // mask, online softmax over the pair's keys (x: unscaled scores)
@@ -962,13 +984,13 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
           // f32: lane (lm, lg) takes V rows key + 4 lg + r at d = 16 db + lm
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
-            const char* vrow = vs + (kb0 * kBlk + 4 * lg) * C::kPitch + h * bstride + 4 * lm;
+            const char* vrow = vs + (kb0 * kBlk + 4 * lg) * C::kPitchV + h * vbstride + 4 * lm;
 #pragma unroll
             for (int db = 0; db < C::kDB; ++db)
 #pragma unroll
               for (int r = 0; r < 4; ++r)
                 o[db] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                    *reinterpret_cast<const float*>(vrow + r * C::kPitch + 64 * db), pr[4 * h + r], o[db], 0, 0, 0);
+                    *reinterpret_cast<const float*>(vrow + r * C::kPitchV + 64 * db), pr[4 * h + r], o[db], 0, 0, 0);
           }
         }
       }
@@ -1007,8 +1029,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         if (active) {
           const int region = rb * nks + kslot;
           f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
+          // the d blocks the other waves of the row block merge (this wave
+          // keeps its own slice in registers)
 #pragma unroll
-          for (int db = 0; db < C::kDB; ++db) reg[db * 64 + lane] = o[db];
+          for (int db = 0; db < C::kDB; ++db)
+            if (db < d_lo || db >= d_hi) reg[db * 64 + lane] = o[db];
           if (lg == 0) {   // the four lanes of a row hold the same values
             mst[region][0][lm] = m_run;
             mst[region][1][lm] = fl;
@@ -1039,7 +1064,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
               for (int k = 0; k < kConsumers; ++k) {
                 if (k < nks) {
                   const f32x4* reg = reinterpret_cast<const f32x4*>(scratch + (rb * nks + k) * (64 * D));
-                  acc += reg[db * 64 + lane] * wk[k];
+                  acc += (k == kslot ? o[db] : reg[db * 64 + lane]) * wk[k];
                 }
               }
               o[db] = acc;
@@ -1058,7 +1083,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       pend_ok = active && row_valid;
       pend_inv = fl > 0.f ? 1.f / fl : 0.f;
       pend_lse = fl > 0.f ? (fm + log2f(fl)) * kLn2 : -INFINITY;
-      pend_row = whole ? (b * p.C_max + tok) * p.Hq + kvh * g + row % g : (2 * pid + (seg_g == g0 ? 0 : 1)) * p.Rcap + row;
+      pend_row = whole ? (b * p.C_max + tok) * p.Hq + kvh * g + row - tok * g
+                       : (2 * pid + (seg_g == g0 ? 0 : 1)) * p.Rcap + row;
       if (!whole) {
         Pub q;
         q.state = 0;
