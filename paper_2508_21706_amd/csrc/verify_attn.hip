@@ -91,6 +91,11 @@ typedef __attribute__((ext_vector_type(4))) int i32x4;
 // data goes through, or around, the XCD-local L2 to the point where every XCD
 // sees it, without an L2-wide write-back or invalidate.
 constexpr int kDeviceCoherent = 16;   // SC1
+// Cache policy of the K/V tile loads: non-temporal (NT).  Every K/V byte is
+// read once, so the stream should not displace the cache lines that are
+// reused (the partial results, the output being written); with the default
+// policy the whole launch ran 6-11% slower.
+constexpr int kStreaming = 2;
 constexpr int kBufferFormat = 0x00020000;   // raw 32-bit buffer descriptor word 3
 
 struct Params {
@@ -623,10 +628,10 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       // scores are masked whatever the slots hold
       if (i < C::kInstK && sl < C::kTileKeys * C::kSlotsK && (64 * i) / C::kSlotsK <= last)
         __builtin_amdgcn_global_load_lds(kp + koff, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
-                                         0);
+                                         kStreaming);
       if (i < C::kInstV && sl < C::kTileKeys * C::kSlotsV)
         __builtin_amdgcn_global_load_lds(vp + voff, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0,
-                                         0);
+                                         kStreaming);
     }
   };
 
