@@ -4,4 +4,4 @@ TEST INFRASTRUCTURE, NOT PART OF THE PRODUCT: only tests, the smoke check and
 the benchmark's CPU-baseline leg may use it.  See ``oracle.reference``.
 """
 from .reference import (bf16_bits_to_f64, chain_mask, chunked_attention,  # noqa: F401
-                              to_f64, verify_attn_ref)
+                        to_f64, tree_mask, verify_attn_ref)

@@ -22,18 +22,32 @@ What it computes is the chunked-attention operator as the paper defines it
 Grouped-query attention follows the paper's group factor g (Section 3.1,
 "Model"): g query heads share one KV head; query head h reads KV head h // g.
 
+Tree drafts (Section 2.3 on speculative decoding; Section 5.1, where only the
+draft part of the mask is stored): the draft tokens of a tree are kept as a
+sequence and an extra mask says which of them each draft token sees.  Here
+that part is one bit word per draft token: bit k of word i set means draft
+token i attends to draft token k (key position l + k).  Cached tokens are
+always visible.
+
 Readings where the paper is silent or garbled:
-the printed mask set {-inf, 1} is read as {-inf, 0}; the draft is a chain, not a
-tree; the cached tokens come first in K/V, the chunk after; the softmax scale
-is an argument; rows of a sequence beyond its chunk length are padding and get
-out = 0, lse = -inf.
+the printed mask set {-inf, 1} is read as {-inf, 0}; without a draft mask the
+draft is a chain; the cached tokens come first in K/V, the chunk after; the
+softmax scale is an argument; rows of a sequence beyond its chunk length are
+padding and get out = 0, lse = -inf.  A draft mask is any set of bits (a tree's
+ancestor sets are the intended use, but nothing requires it); bits k >= n are
+ignored; a row that sees no key at all (l = 0 and no bit below n) gets out = 0,
+lse = -inf, as a padding row does.
 
 Parity pins (tests/test_oracle.py): a hand-worked golden example, the closed
 form for q = 0 (uniform weights: lse = ln(l+i+1), out = mean of the visible V
 rows), decode attention for n = 1 and full causal attention over the
 concatenated sequence through torch's fp64 CPU scaled-dot-product attention,
 n sequential decode steps, GQA equal to MHA with repeated KV heads, and
-convex-hull / lse-bound / permutation invariants.
+convex-hull / lse-bound / permutation invariants.  Draft masks: a chain's
+words reproduce the chain mask, each row of a tree equals the chain
+attention over its root path, arbitrary masks match torch's fp64 attention
+with a boolean mask, q = 0 gives ln(#visible), and the all-ones mask is
+bidirectional attention.
 """
 from __future__ import annotations
 
@@ -72,6 +86,22 @@ def chain_mask(l: int, n: int) -> np.ndarray:
     return M
 
 
+def tree_mask(l: int, n: int, words) -> np.ndarray:
+    """Additive mask M in {-inf, 0}^{n x (l+n)} of a tree draft (Section 5.1).
+
+    Every draft token sees all l cached tokens; draft token i sees draft token
+    k (key position l + k) when bit k of ``words[i]`` is set.  Bits k >= n are
+    ignored.
+    """
+    M = np.full((n, l + n), -np.inf)
+    M[:, :l] = 0.0
+    for i in range(n):
+        for k in range(n):
+            if (int(words[i]) >> k) & 1:
+                M[i, l + k] = 0.0
+    return M
+
+
 def chunked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, M: np.ndarray,
                       scale: float):
     """One sequence, one query head: out = softmax(scale * Q K^T + M) V.
@@ -79,19 +109,24 @@ def chunked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, M: np.ndarray
     Q [n, d], K and V [l+n, d], M [n, l+n], all float64.  Returns out [n, d]
     and lse [n] (natural log of each row's softmax denominator).  The softmax
     subtracts the row maximum before exponentiating, which leaves the result
-    unchanged and keeps exp() in range.
+    unchanged and keeps exp() in range.  A row whose mask hides every key
+    keeps out = 0, lse = -inf.
     """
+    out = np.zeros((Q.shape[0], V.shape[1]))
+    lse = np.full(Q.shape[0], -np.inf)
+    seen = np.isfinite(M).any(axis=1)        # rows that see at least one key
     S = scale * (Q @ K.T) + M
+    S = S[seen]
     m = S.max(axis=1, keepdims=True)
     E = np.exp(S - m)
     Z = E.sum(axis=1, keepdims=True)
-    out = (E / Z) @ V
-    lse = (m + np.log(Z))[:, 0]
+    out[seen] = (E / Z) @ V
+    lse[seen] = (m + np.log(Z))[:, 0]
     return out, lse
 
 
 def verify_attn_ref(q, k_cache, v_cache, ctx_lens, chunk_lens, scale: float,
-                    dtype: str, units=None):
+                    dtype: str, units=None, draft_mask=None):
     """Chunked verification attention for a batch of sequences, in float64.
 
     q        [B, C_max, Hq, D]      queries of each sequence's draft chunk
@@ -101,6 +136,8 @@ def verify_attn_ref(q, k_cache, v_cache, ctx_lens, chunk_lens, scale: float,
     dtype    "bf16" (uint16 bit patterns) or "f32"
     units    optional iterable of (b, kv_head) pairs to compute; the others
              are left NaN (for sampled checks of large workloads)
+    draft_mask  optional integer array [B, C_max] of draft-mask words (see
+             tree_mask); None means a chain draft (chain_mask)
 
     Returns out [B, C_max, Hq, D] and lse [B, C_max, Hq] in float64.  Padding
     rows (i >= c_b) of computed units hold out = 0, lse = -inf.
@@ -119,7 +156,7 @@ def verify_attn_ref(q, k_cache, v_cache, ctx_lens, chunk_lens, scale: float,
         n = int(chunk_lens[b])
         K = to_f64(k_cache[b, kvh, : l + n], dtype)
         V = to_f64(v_cache[b, kvh, : l + n], dtype)
-        M = chain_mask(l, n)
+        M = chain_mask(l, n) if draft_mask is None else tree_mask(l, n, draft_mask[b])
         for h in range(kvh * g, (kvh + 1) * g):
             out[b, n:, h] = 0.0
             lse[b, n:, h] = -np.inf

@@ -12,7 +12,7 @@ attend to l cached tokens plus the chunk itself.  The KV cache is the paper's
 [l_b, l_b + c_b) the chunk's own K/V, already appended.  Queries are
 token-major [B, C_max, Hq, D].
 
-The five workloads stand in for the paper's APPS and CNN/DailyMail runs of
+The workloads stand in for the paper's APPS and CNN/DailyMail runs of
 Mixtral-8x7B (Section 6.1, dataset table): those datasets and model weights are
 not used; lengths are drawn from distributions that cover their prefix lengths
 (APPS mean 566 input tokens plus up to 1024 generated; CNN/DM mean 1006), and
@@ -31,6 +31,13 @@ Recipe (all draws with numpy's PCG64 ``default_rng``):
     same bits feed the GPU and the oracle.
   * Rows that hold no valid data (cache rows >= T_b, query rows >= c_b) are
     filled with ``fill`` (NaN by default) so that any read of them shows up.
+  * Tree drafts (workloads with ``draft="tree"``): the draft tokens of
+    sequence b form a random recursive tree drawn with
+    ``default_rng([seed, 3, b])``: token 0 is the root and token i >= 1 hangs
+    under a parent drawn uniformly from the tokens before it.  The tree is
+    handed over as draft-mask words: word i has bit k set for every token k
+    on the path from the root to i (i itself included).  Words of rows
+    i >= c_b are 0.
 """
 from __future__ import annotations
 
@@ -55,6 +62,7 @@ class Workload:
     ctx: tuple            # ("fixed", [..]) | ("uniform", lo, hi) | ("loguniform", lo, hi)
     chunk: tuple          # ("fixed", n) | ("uniform", lo, hi)
     description: str
+    draft: str = "chain"  # "chain", or "tree": a random tree with draft-mask words
 
     @property
     def group(self) -> int:
@@ -106,6 +114,10 @@ WORKLOADS = [
              ctx=("uniform", 256, 4096), chunk=("uniform", 1, 16),
              description="ragged chunks, wide GQA, bf16: B=128, Hq=28, Hkv=4, D=128, "
                          "ctx U[256,4096], chunk U[1,16]"),
+    Workload("mixtral_tree_b64", 6, B=64, Hq=32, Hkv=8, D=128, dtype="bf16",
+             ctx=("uniform", 512, 2048), chunk=("fixed", 16), draft="tree",
+             description="Mixtral-8x7B attention shape with 16-token tree drafts, bf16: B=64, Hq=32, "
+                         "Hkv=8, D=128, ctx U[512,2048], chunk 16, random recursive trees"),
 ]
 BY_NAME = {w.name: w for w in WORKLOADS}
 
@@ -179,7 +191,8 @@ def make_inputs(w: Workload, fill: float = float("nan"),
 
     Returns a dict with q [B, C_max, Hq, D], k_cache / v_cache
     [B, Hkv, S_max, D] (uint16 bf16 bits, or float32), ctx_lens, chunk_lens
-    (int32 [B]), scale, and the workload itself.  ``batches`` restricts the
+    (int32 [B]), scale, the workload itself, and draft_mask (uint64
+    [B, C_max] words of a tree workload, else None).  ``batches`` restricts the
     cache fill to those sequences (others keep ``fill``), for sampled checks of
     large workloads.  ``ctx_lens`` / ``chunk_lens`` override the drawn lengths.
     """
@@ -204,8 +217,51 @@ def make_inputs(w: Workload, fill: float = float("nan"),
         T_b = int(ctx[b]) + int(chunk[b])
         k[b, :, :T_b] = kv_slab(w, b, T_b, "k")
         v[b, :, :T_b] = kv_slab(w, b, T_b, "v")
+    draft_mask = tree_draft_masks(w.index, chunk, w.C_max) if w.draft == "tree" else None
     return dict(q=q, k_cache=k, v_cache=v, ctx_lens=ctx, chunk_lens=chunk,
-                scale=w.scale, workload=w)
+                scale=w.scale, workload=w, draft_mask=draft_mask)
+
+
+def tree_draft_masks(seed: int, chunk_lens, C_max: int) -> np.ndarray:
+    """Draft-mask words [B, C_max] (uint64) of random recursive trees.
+
+    Sequence b's tree comes from ``default_rng([seed, 3, b])``: token 0 is the
+    root, token i >= 1 gets a parent drawn uniformly from 0..i-1, and word i
+    holds the bits of the tokens on the root path of i, i itself included.
+    Rows i >= c_b hold 0.
+    """
+    chunk = np.asarray(chunk_lens, np.int64)
+    if C_max > 64:
+        raise ValueError("draft-mask words hold at most 64 draft tokens")
+    words = np.zeros((len(chunk), C_max), np.uint64)
+    for b, n in enumerate(chunk):
+        rng = np.random.default_rng([seed, 3, b])
+        for i in range(int(n)):
+            own = np.uint64(1) << np.uint64(i)
+            words[b, i] = own if i == 0 else words[b, int(rng.integers(0, i))] | own
+    return words
+
+
+def random_draft_masks(rng: np.random.Generator, chunk_lens, C_max: int, density: float = 0.5,
+                       self_bit: bool = True, junk_high_bits: bool = False) -> np.ndarray:
+    """Arbitrary draft-mask words [B, C_max] (uint64), for edge cases.
+
+    Each bit k < c_b of word i < c_b is set with probability ``density``;
+    ``self_bit`` forces bit i of word i.  ``junk_high_bits`` also sets random
+    bits k >= c_b, which the operator must ignore.  Rows i >= c_b hold 0.
+    """
+    chunk = np.asarray(chunk_lens, np.int64)
+    words = np.zeros((len(chunk), C_max), np.uint64)
+    for b, n in enumerate(chunk):
+        n = int(n)
+        for i in range(n):
+            bits = rng.random(64) < density
+            if not junk_high_bits:
+                bits[n:] = False
+            if self_bit:
+                bits[i] = True
+            words[b, i] = np.uint64(int(sum(1 << k for k in range(64) if bits[k])))
+    return words
 
 
 def algorithmic_kv_bytes(w: Workload, ctx_lens, chunk_lens) -> int:

@@ -255,9 +255,128 @@ def pin_bf16_path(m):
     np.testing.assert_array_equal(s1, s2)
 
 
+# ------------------------------------------------------- draft-mask pins
+
+def _chain_words(n):
+    return [(1 << (i + 1)) - 1 for i in range(n)]
+
+
+def pin_tree_chain_words_are_causal(m):
+    """The words of a chain (token i sees tokens 0..i) reproduce the chain
+    mask: a tree draft that happens to be a sequence is the plain case."""
+    rng = np.random.default_rng(21)
+    q, k, v, ctx, chunk = _rand_case(rng, ctx=(7, 0), chunk=(5, 3), C_max=6)
+    words = np.zeros((2, 6), np.uint64)
+    for b in range(2):
+        words[b, : chunk[b]] = _chain_words(int(chunk[b]))
+    o1, s1 = m.verify_attn_ref(q, k, v, ctx, chunk, 0.3, "f32")
+    o2, s2 = m.verify_attn_ref(q, k, v, ctx, chunk, 0.3, "f32", draft_mask=words)
+    np.testing.assert_array_equal(o1, o2)
+    np.testing.assert_array_equal(s1, s2)
+
+
+def pin_tree_row_is_its_root_path(m):
+    """In a tree draft, token i attends to the cached tokens and its root path
+    only, so its row equals the last row of a chain draft made of that path
+    (Section 2.3: the tree's tokens are kept as a sequence plus a mask)."""
+    rng = np.random.default_rng(22)
+    B, Hq, Hkv, D, C = 3, 4, 2, 8, 9
+    ctx = np.array([6, 0, 11], np.int32)
+    chunk = np.array([9, 7, 4], np.int32)
+    q, k, v, _, _ = _rand_case(rng, B=B, Hq=Hq, Hkv=Hkv, D=D, ctx=ctx, chunk=chunk, C_max=C)
+    words = wl.tree_draft_masks(5, chunk, C)
+    o, s = m.verify_attn_ref(q, k, v, ctx, chunk, 0.45, "f32", draft_mask=words)
+    for b in range(B):
+        l = int(ctx[b])
+        assert np.all(o[b, chunk[b]:] == 0.0) and np.all(s[b, chunk[b]:] == -np.inf)
+        for i in range(int(chunk[b])):
+            path = [t for t in range(int(chunk[b])) if (int(words[b, i]) >> t) & 1]
+            assert path[-1] == i and path[0] == 0
+            rows = list(range(l)) + [l + t for t in path]
+            kp = k[b:b + 1, :, rows]
+            vp = v[b:b + 1, :, rows]
+            qp = np.zeros((1, len(path), Hq, D), np.float32)
+            qp[0, -1] = q[b, i]
+            o1, s1 = m.verify_attn_ref(qp, kp, vp, np.array([l], np.int32),
+                                       np.array([len(path)], np.int32), 0.45, "f32")
+            np.testing.assert_allclose(o[b, i], o1[0, -1], rtol=0, atol=1e-12)
+            np.testing.assert_allclose(s[b, i], s1[0, -1], rtol=0, atol=1e-12)
+
+
+def pin_tree_matches_sdpa_boolean_mask(m):
+    """Arbitrary draft masks (not trees) against torch's fp64 attention with a
+    boolean mask over the l + n keys."""
+    rng = np.random.default_rng(23)
+    B, Hq, Hkv, D, C = 2, 6, 3, 16, 7
+    ctx = np.array([5, 13], np.int32)
+    chunk = np.array([7, 4], np.int32)
+    q, k, v, _, _ = _rand_case(rng, B=B, Hq=Hq, Hkv=Hkv, D=D, ctx=ctx, chunk=chunk, C_max=C)
+    words = wl.random_draft_masks(rng, chunk, C, density=0.4, self_bit=False, junk_high_bits=True)
+    o, s = m.verify_attn_ref(q, k, v, ctx, chunk, 0.21, "f32", draft_mask=words)
+    g = Hq // Hkv
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float64))[None, None]
+    for b in range(B):
+        l, n = int(ctx[b]), int(chunk[b])
+        allow = np.ones((n, l + n), bool)
+        for i in range(n):
+            for kk in range(n):
+                allow[i, l + kk] = bool((int(words[b, i]) >> kk) & 1)
+        for h in range(Hq):
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                t(q[b, :n, h]), t(k[b, h // g, :l + n]), t(v[b, h // g, :l + n]),
+                attn_mask=torch.from_numpy(allow)[None, None], scale=0.21)[0, 0].numpy()
+            np.testing.assert_allclose(o[b, :n, h], ref, rtol=0, atol=1e-12)
+
+
+def pin_tree_uniform_closed_form(m):
+    """q = 0 under a draft mask: lse = ln(l + #set bits below n), out = mean
+    of the visible V rows; with l = 0 an empty word leaves the row without
+    keys (out 0, lse -inf).  Bits at or above n do not count."""
+    rng = np.random.default_rng(24)
+    B, Hq, Hkv, D, C = 3, 2, 1, 4, 6
+    ctx = np.array([0, 3, 0], np.int32)
+    chunk = np.array([6, 5, 2], np.int32)
+    q, k, v, _, _ = _rand_case(rng, B=B, Hq=Hq, Hkv=Hkv, D=D, ctx=ctx, chunk=chunk, C_max=C)
+    q[:] = 0.0
+    words = np.zeros((B, C), np.uint64)
+    words[0, :6] = [0b000001, 0, 0b101101, 0b111111, 0b010000 | (1 << 40), 1 << 63]
+    words[1, :5] = [0, 0b10110, 0b11111, 0b01000, 1 << 5]
+    words[2, :2] = [0b10, 0b100]
+    o, s = m.verify_attn_ref(q, k, v, ctx, chunk, 0.8, "f32", draft_mask=words)
+    for b in range(B):
+        l, n = int(ctx[b]), int(chunk[b])
+        for i in range(n):
+            vis = list(range(l)) + [l + t for t in range(n) if (int(words[b, i]) >> t) & 1]
+            for h in range(Hq):
+                if not vis:
+                    assert s[b, i, h] == -np.inf and np.all(o[b, i, h] == 0.0)
+                    continue
+                assert abs(s[b, i, h] - math.log(len(vis))) < 1e-12
+                mean = v[b, 0, vis].astype(np.float64).mean(axis=0)
+                np.testing.assert_allclose(o[b, i, h], mean, rtol=0, atol=1e-12)
+    assert s[0, 1, 0] == -np.inf and s[0, 5, 0] == -np.inf and s[2, 1, 0] == -np.inf
+
+
+def pin_tree_all_ones_is_bidirectional(m):
+    """Every bit set: each draft token sees all l + n keys, which is
+    attention without a mask."""
+    rng = np.random.default_rng(25)
+    q, k, v, ctx, chunk = _rand_case(rng, ctx=(4, 9), chunk=(3, 5), C_max=5, D=16)
+    words = np.full((2, 5), np.uint64(2 ** 64 - 1))
+    o, s = m.verify_attn_ref(q, k, v, ctx, chunk, 0.3, "f32", draft_mask=words)
+    g = q.shape[2] // k.shape[1]
+    for b in range(2):
+        T = int(ctx[b] + chunk[b])
+        for h in range(q.shape[2]):
+            ref = _sdpa(q[b, : chunk[b], h], k[b, h // g, :T], v[b, h // g, :T], 0.3, causal=False)
+            np.testing.assert_allclose(o[b, : chunk[b], h], ref, rtol=0, atol=1e-12)
+
+
 PINS = [pin_bf16_decoding, pin_hand_example, pin_uniform_closed_form, pin_decode_is_sdpa,
         pin_chunk_is_causal_prefill, pin_sequential_decode, pin_gqa_is_repeated_mha,
-        pin_invariants, pin_one_hot, pin_padding_and_poison, pin_bf16_path]
+        pin_invariants, pin_one_hot, pin_padding_and_poison, pin_bf16_path,
+        pin_tree_chain_words_are_causal, pin_tree_row_is_its_root_path, pin_tree_matches_sdpa_boolean_mask,
+        pin_tree_uniform_closed_form, pin_tree_all_ones_is_bidirectional]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda p: p.__name__)
@@ -272,8 +391,8 @@ MUTATIONS = {
     "mask_leaks_next": ("M[i, : l + i + 1] = 0.0", "M[i, : l + i + 2] = 0.0"),
     "mask_context_only": ("M[i, : l + i + 1] = 0.0", "M[i, : l + 1] = 0.0"),
     "no_scale": ("S = scale * (Q @ K.T) + M", "S = (Q @ K.T) + M"),
-    "lse_drops_max": ("lse = (m + np.log(Z))[:, 0]", "lse = np.log(Z)[:, 0]"),
-    "unnormalised": ("out = (E / Z) @ V", "out = E @ V"),
+    "lse_drops_max": ("lse[seen] = (m + np.log(Z))[:, 0]", "lse[seen] = np.log(Z)[:, 0]"),
+    "unnormalised": ("out[seen] = (E / Z) @ V", "out[seen] = E @ V"),
     "gqa_modulo": ("for h in range(kvh * g, (kvh + 1) * g):", "for h in range(kvh, Hq, Hkv):"),
     "k_shifted": ("K = to_f64(k_cache[b, kvh, : l + n], dtype)",
                   "K = to_f64(k_cache[b, kvh, 1 : l + n + 1], dtype)"),
@@ -282,7 +401,16 @@ MUTATIONS = {
     "bf16_shift": ("<< np.uint32(16)", "<< np.uint32(15)"),
     "padding_lse_zero": ("lse[b, n:, h] = -np.inf", "lse[b, n:, h] = 0.0"),
     "q_wrong_token": ("Q = to_f64(q[b, :n, h], dtype)", "Q = to_f64(q[b, 1 : n + 1, h], dtype)"),
-    "transposed_scores": ("out = (E / Z) @ V", "out = (E / Z) @ V[::-1]"),
+    "transposed_scores": ("out[seen] = (E / Z) @ V", "out[seen] = (E / Z) @ V[::-1]"),
+    "tree_bits_reversed": ("if (int(words[i]) >> k) & 1:", "if (int(words[i]) >> (n - 1 - k)) & 1:"),
+    "tree_transposed": ("if (int(words[i]) >> k) & 1:", "if (int(words[k]) >> i) & 1:"),
+    "tree_no_offset": ("M[i, l + k] = 0.0", "M[i, k] = 0.0"),
+    "tree_context_hidden": ("M[:, :l] = 0.0", "M[:, : max(l - 1, 0)] = 0.0"),
+    "tree_high_bits_count": ("        for k in range(n):\n            if (int(words[i])",
+                             "        for k in range(n):\n            if k == n - 1 or (int(words[i])"),
+    "dead_row_lse_zero": ("lse = np.full(Q.shape[0], -np.inf)", "lse = np.zeros(Q.shape[0])"),
+    "tree_ignored": ("M = chain_mask(l, n) if draft_mask is None else tree_mask(l, n, draft_mask[b])",
+                     "M = chain_mask(l, n)"),
 }
 
 
@@ -367,3 +495,30 @@ def test_kv_accounting_matches_paper_cost_model():
         assert per_layer == 2 * batch * s * h // g * vals["elt_bytes"]
         total_gib = per_layer * vals["layers"] / 2 ** 30
         assert abs(total_gib - gib) / gib < 1e-3, total_gib
+
+
+def test_tree_masks_are_root_paths():
+    """The tree recipe's words are root paths of a tree: word i holds bit i,
+    bits only at or below i, and removing bit i leaves the word of i's parent
+    (its highest remaining bit); rows past c_b are 0; draws repeat."""
+    chunk = np.array([16, 1, 0, 9], np.int32)
+    words = wl.tree_draft_masks(6, chunk, 16)
+    assert words.dtype == np.uint64 and words.shape == (4, 16)
+    for b, n in enumerate(chunk):
+        for i in range(16):
+            w = int(words[b, i])
+            if i >= n:
+                assert w == 0
+                continue
+            assert (w >> i) & 1 and w < (1 << (i + 1))
+            if i == 0:
+                assert w == 1
+            else:
+                rest = w & ~(1 << i)
+                parent = rest.bit_length() - 1
+                assert 0 <= parent < i and int(words[b, parent]) == rest
+    assert np.array_equal(words, wl.tree_draft_masks(6, chunk, 16))
+    w6 = wl.get("mixtral_tree_b64")
+    inp = wl.make_inputs(wl.dataclasses.replace(w6, B=2), batches=[])
+    assert inp["draft_mask"].shape == (2, 16) and inp["draft_mask"][0, 0] == 1
+    assert wl.make_inputs(wl.dataclasses.replace(wl.get(1)))["draft_mask"] is None
