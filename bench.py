@@ -75,7 +75,7 @@ def cpu_baseline(inp, w, budget_s: float):
         units = [(b, h) for h in range(w.Hkv)]
         t0 = time.perf_counter()
         verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], inp["ctx_lens"], inp["chunk_lens"],
-                        w.scale, w.dtype, units=units)
+                        w.scale, w.dtype, units=units, draft_mask=inp["draft_mask"])
         t_total += time.perf_counter() - t0
         done.append(b)
     ctx = inp["ctx_lens"][done]
@@ -140,8 +140,10 @@ def main():
     g = w.group
     elt = w.elt_bytes
     # algorithmic bytes of one main-kernel launch: K+V of valid rows, the valid
-    # query rows, and the fp32 out + lse rows it produces
-    launch_bytes = kv_bytes + int(chunk.sum()) * w.Hq * (w.D * elt + (w.D + 1) * 4)
+    # query rows, and the fp32 out + lse rows it produces (tree drafts: plus
+    # the 8-byte draft-mask word of every valid row)
+    tree = inp["draft_mask"] is not None
+    launch_bytes = kv_bytes + int(chunk.sum()) * (w.Hq * (w.D * elt + (w.D + 1) * 4) + (8 if tree else 0))
 
     def to_dev(a):
         if w.dtype == "bf16":
@@ -155,6 +157,7 @@ def main():
     sets = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_sets - 1)]
     ctx_d = torch.from_numpy(ctx).to(dev)
     chunk_d = torch.from_numpy(chunk).to(dev)
+    mask_d = torch.from_numpy(inp["draft_mask"].view(np.int64)).to(dev) if tree else None
     desc = pkg.desc_for(q, k0, args.grid_blocks)
     ws = pkg.alloc_workspace(desc, dev)
     out = torch.empty((w.B, w.C_max, w.Hq, w.D), dtype=torch.float32, device=dev)
@@ -165,8 +168,12 @@ def main():
 
     def step(i, events=None):
         k, v = sets[i % n_sets]
-        pkg.verify_attn(q, k, v, ctx_d, chunk_d, w.scale, out=out, lse=lse, workspace=ws,
-                        grid_blocks=args.grid_blocks, stream=stream, events=events)
+        if tree:
+            pkg.verify_attn_tree(q, k, v, ctx_d, chunk_d, mask_d, w.scale, out=out, lse=lse, workspace=ws,
+                                 grid_blocks=args.grid_blocks, stream=stream, events=events)
+        else:
+            pkg.verify_attn(q, k, v, ctx_d, chunk_d, w.scale, out=out, lse=lse, workspace=ws,
+                            grid_blocks=args.grid_blocks, stream=stream, events=events)
 
     # settle: sustained load until the GPU runs at its working clock (a short
     # warmup alone measures the ramp: about 5% slower on this workload)
@@ -242,7 +249,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
                    "head_dim": w.D, "ctx_lens_sum": int(ctx.sum()), "chunk_lens_sum": tokens,
-                   "C_max": w.C_max, "S_max": w.S_max, "grid_blocks": args.grid_blocks or 256,
+                   "C_max": w.C_max, "S_max": w.S_max, "draft": w.draft,
+                   "grid_blocks": args.grid_blocks or 256,
                    "input_sets": n_sets,
                    "parallelism": "single GPU"},
         "verified_tokens_per_s": round(tokens / t, 1),

@@ -35,7 +35,7 @@ typedef enum {
   SPECMOE_BF16 = 1
 } specmoe_dtype;
 
-/* Status codes returned by specmoe_verify_attn (0 = success). */
+/* Status codes returned by the entry points (0 = success). */
 enum {
   SPECMOE_OK = 0,
   SPECMOE_ERR_NULL_POINTER = -1,  /* a required pointer (or the descriptor) is NULL   */
@@ -49,10 +49,12 @@ enum {
                                      large that partial results would pass 2 GB       */
   SPECMOE_ERR_WORKSPACE = -8,     /* workspace smaller than the size query returns    */
   SPECMOE_ERR_ALIGN = -9,         /* q, k_cache, v_cache, out or workspace is not
-                                     16-byte aligned                                  */
+                                     16-byte aligned, or draft_mask not 8-byte aligned */
   SPECMOE_ERR_SCALE = -10,        /* scale is not finite                              */
   SPECMOE_ERR_LAUNCH = -11,       /* HIP reported an error for a kernel launch        */
-  SPECMOE_ERR_FLAGS = -12         /* flags is not 0                                   */
+  SPECMOE_ERR_FLAGS = -12,        /* flags is not 0                                   */
+  SPECMOE_ERR_MASK = -13          /* a draft mask with C_max > 64 (one 64-bit word per
+                                     draft token covers at most 64 draft tokens)      */
 };
 
 /* Problem description.  Sizes are in elements unless stated otherwise. */
@@ -130,6 +132,37 @@ int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
                         const int32_t* ctx_lens, const int32_t* chunk_lens,
                         float scale, float* out, float* lse, void* stream,
                         const specmoe_verify_desc* desc);
+
+/*
+ * specmoe_verify_attn_tree -- chunked verification attention for tree drafts.
+ *
+ * The same operation as specmoe_verify_attn, except inside the draft region:
+ * when the draft tokens form a tree (Section 2.3: a tree of draft tokens is
+ * verified as a sequence plus a mask relating them), the draft part of the
+ * mask is given explicitly, and only that part (Section 5.1 stores only the
+ * draft region of the mask; the cached part is always visible):
+ *
+ *   draft_mask  uint64 [B, C_max], device, 8-byte aligned.  Bit k of
+ *               draft_mask[b * C_max + i] is set when draft token i of
+ *               sequence b attends to draft token k, i.e. key position
+ *               l_b + k.  Every cached key j < l_b is visible to every draft
+ *               token.  Bits k >= c_b are ignored, words of rows i >= c_b are
+ *               never read.  For a tree, word i holds the tokens on the path
+ *               from the root to i (i included); a chain draft's word i is
+ *               2^(i+1) - 1, which reproduces specmoe_verify_attn.  Any other
+ *               bit pattern is allowed.
+ *
+ * A draft token that sees no key (l_b = 0 and no bit below c_b) gets out = 0
+ * and lse = -inf, as a padding row does.  C_max must be <= 64
+ * (SPECMOE_ERR_MASK otherwise); a NULL draft_mask is SPECMOE_ERR_NULL_POINTER
+ * and a misaligned one SPECMOE_ERR_ALIGN (with B > 0).  Every other argument,
+ * the workspace, the preconditions, ownership, determinism and the errors are
+ * those of specmoe_verify_attn; the two entry points can share a workspace.
+ */
+int specmoe_verify_attn_tree(const void* q, const void* k_cache, const void* v_cache,
+                             const int32_t* ctx_lens, const int32_t* chunk_lens,
+                             const uint64_t* draft_mask, float scale, float* out, float* lse,
+                             void* stream, const specmoe_verify_desc* desc);
 
 /* Bytes of device workspace specmoe_verify_attn needs for `desc` (its
  * grid_blocks included); 0 for an invalid descriptor.  The workspace starts

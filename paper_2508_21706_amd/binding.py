@@ -23,7 +23,7 @@ STATUS = {
     0: "SPECMOE_OK", -1: "SPECMOE_ERR_NULL_POINTER", -2: "SPECMOE_ERR_SHAPE", -3: "SPECMOE_ERR_GQA",
     -4: "SPECMOE_ERR_HEAD_DIM", -5: "SPECMOE_ERR_DTYPE", -6: "SPECMOE_ERR_ROWS", -7: "SPECMOE_ERR_GRID",
     -8: "SPECMOE_ERR_WORKSPACE", -9: "SPECMOE_ERR_ALIGN", -10: "SPECMOE_ERR_SCALE", -11: "SPECMOE_ERR_LAUNCH",
-    -12: "SPECMOE_ERR_FLAGS",
+    -12: "SPECMOE_ERR_FLAGS", -13: "SPECMOE_ERR_MASK",
 }
 
 
@@ -60,6 +60,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.specmoe_verify_attn.restype = ctypes.c_int
     lib.specmoe_verify_attn.argtypes = [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_tree.restype = ctypes.c_int
+    lib.specmoe_verify_attn_tree.argtypes = [
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Desc)]
     lib.specmoe_verify_attn_workspace_bytes.restype = ctypes.c_size_t
     lib.specmoe_verify_attn_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
@@ -153,6 +157,30 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     preconditions; off by default.  Repeated calls with the same inputs and
     grid give bitwise-identical results.
     """
+    return _call(q, k_cache, v_cache, ctx_lens, chunk_lens, None, scale, out, lse, workspace, grid_blocks,
+                 stream, events, check_lengths)
+
+
+def verify_attn_tree(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                     ctx_lens: torch.Tensor, chunk_lens: torch.Tensor, draft_mask: torch.Tensor, scale: float,
+                     out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
+                     stream: Optional[torch.cuda.Stream] = None, events=None,
+                     check_lengths: bool = False):
+    """Chunked verification attention for tree drafts; see
+    ``specmoe_verify_attn_tree`` in ``include/specmoe_verify.h``.
+
+    Arguments as ``verify_attn``, plus ``draft_mask``: int64 (or uint64)
+    [B, C_max] on the GPU, the 64-bit draft-mask words (bit k of word
+    [b, i] set: draft token i of sequence b attends to draft token k).
+    C_max must be <= 64.
+    """
+    return _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse, workspace,
+                 grid_blocks, stream, events, check_lengths)
+
+
+def _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse, workspace, grid_blocks,
+          stream, events, check_lengths):
     lib = load_library()
     B, C_max, Hq, D = q.shape
     if k_cache.dim() != 4:
@@ -164,6 +192,9 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     _check(v_cache, "v_cache", (B, Hkv, S_max, D), dt)
     _check(ctx_lens, "ctx_lens", (B,), torch.int32)
     _check(chunk_lens, "chunk_lens", (B,), torch.int32)
+    if draft_mask is not None:
+        mdt = draft_mask.dtype if draft_mask.dtype in (torch.int64, torch.uint64) else torch.int64
+        _check(draft_mask, "draft_mask", (B, C_max), mdt)
     if check_lengths:
         c = chunk_lens.cpu()
         l = ctx_lens.cpu()
@@ -185,9 +216,15 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     desc.workspace_bytes = workspace.numel() * workspace.element_size()
     if events is not None:
         desc.ev_main_begin, desc.ev_main_end = events
-    st = lib.specmoe_verify_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
-                                 ctx_lens.data_ptr(), chunk_lens.data_ptr(), float(scale),
-                                 out.data_ptr(), lse.data_ptr(), s.cuda_stream, ctypes.byref(desc))
+    if draft_mask is None:
+        st = lib.specmoe_verify_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                     ctx_lens.data_ptr(), chunk_lens.data_ptr(), float(scale),
+                                     out.data_ptr(), lse.data_ptr(), s.cuda_stream, ctypes.byref(desc))
+    else:
+        st = lib.specmoe_verify_attn_tree(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                          ctx_lens.data_ptr(), chunk_lens.data_ptr(), draft_mask.data_ptr(),
+                                          float(scale), out.data_ptr(), lse.data_ptr(), s.cuda_stream,
+                                          ctypes.byref(desc))
     if st != 0:
         raise SpecMoEError(st, status_str(st))
     return out, lse

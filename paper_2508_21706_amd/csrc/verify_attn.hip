@@ -73,6 +73,7 @@ constexpr int kMaxRows = 128;                 // row blocks per unit <= 8
 constexpr int kDefaultGrid = 256;             // persistent workgroups: one per CU of an MI355X
 constexpr int kMaxGrid = 2048;
 constexpr int kMaxSeqs = 1024;                // sequences per launch (their lengths live in LDS)
+constexpr int kMaxDraftBits = 64;             // draft tokens a draft-mask word covers
 constexpr float kLog2e = 1.4426950408889634f;
 // The running max is only raised when a block's max exceeds it by more than
 // this (log2 units): probabilities stay <= 2^8, and the O rescale is skipped
@@ -114,6 +115,7 @@ struct Params {
   int Rcap;         // C_max * g
   int P;            // persistent workgroups
   float sl2;        // scale * log2(e)
+  const uint64_t* draft_mask;   // [B][C_max] draft-mask words (tree drafts only)
 };
 
 template <bool BF16, int D>
@@ -384,8 +386,9 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
 #pragma unroll
     for (int it = 0; it < kItems; ++it) {
       if (base + it * kCThreads >= n_items) continue;
-      *reinterpret_cast<f32x4*>(p.out + orow[it] * D + d0[it]) = acc[it] * (1.f / z[it]);
-      if (d0[it] == 0) p.lse[orow[it]] = m[it] + logf(z[it]);
+      // (z = 0: a row that sees no key in any piece)
+      *reinterpret_cast<f32x4*>(p.out + orow[it] * D + d0[it]) = acc[it] * (z[it] > 0.f ? 1.f / z[it] : 0.f);
+      if (d0[it] == 0) p.lse[orow[it]] = z[it] > 0.f ? m[it] + logf(z[it]) : -INFINITY;
     }
   }
   if (ctid == 0) {   // ready for the next call
@@ -394,7 +397,9 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
   }
 }
 
-template <bool BF16, int D>
+// TREE: the draft region obeys per-token draft-mask words instead of the
+// chain mask.
+template <bool BF16, int D, bool TREE>
 __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   using C = Cfg<BF16, D>;
   __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
@@ -646,6 +651,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // merging the waves' partial states at the end of every unit.
   int R = 0, n_rbp = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
   bool active = false, row_valid = false;
+  uint64_t tmask = 0;   // (tree drafts) this lane's row: bit k = sees draft key l_ctx + k
   // x / g for a row 0 <= x < 128 of a unit, by a float reciprocal: exact
   // there, as (x + 1/2) / g lies at least 1 / (2 g) from an integer
   const float inv_g = 1.f / (float)g;
@@ -665,7 +671,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     row = rb * kBlk + lm;
     row_valid = active && row < R;
     tok = row_valid ? div_g(row) : 0;
-    vis = row_valid ? l_ctx + tok : 0x7fffffff;   // last visible key of this lane's row
+    if constexpr (TREE) {
+      // every key below the sequence end passes the compare; the draft
+      // keys are then filtered by the row's word
+      vis = 0x7fffffff;
+      tmask = row_valid ? p.draft_mask[cu.b * p.C_max + tok] : 0;
+    } else {
+      vis = row_valid ? l_ctx + tok : 0x7fffffff;   // last visible key of this lane's row
+    }
   };
   // Q chunks of this lane's row for the unit of cu (zero for invalid rows):
   // chunk 4J + lg of the row feeds the J-th score MFMA.  Consumers only.
@@ -951,6 +964,24 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
             mx = fmaxf(mx, xv);
           }
         }
+        if constexpr (TREE) {
+          // a pair that reaches the draft region (the same for the whole
+          // wave): key l_ctx + k is hidden unless bit k of the row's word is
+          // set.  Keys past the tile's end are already hidden, and a key
+          // that passed the compare has k < c_b <= 64.
+          if (key1 + kBlk > l_ctx) {
+            mx = -INFINITY;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int k = (h == 0 ? key0 : key1) + 4 * lg + r - l_ctx;
+                if (k >= 0 && !((tmask >> (k & 63)) & 1u)) x[4 * h + r] = -INFINITY;
+                mx = fmaxf(mx, x[4 * h + r]);
+              }
+            }
+          }
+        }
         mx = row_max(mx) * p.sl2;   // the scale is positive: max of the scaled scores
         // raise the running max only when the pair's max passes it by
         // more than kLazyMax; the four lanes of a row decide alike
@@ -1191,7 +1222,7 @@ Plan make_plan(const specmoe_verify_desc* d) {
   return pl;
 }
 
-template <bool BF16, int D>
+template <bool BF16, int D, bool TREE>
 void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_desc* d) {
   using C = Cfg<BF16, D>;
   const int B = p.B;
@@ -1206,14 +1237,77 @@ void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_d
     s.v = p.v + slab;
     s.ctx_lens = p.ctx_lens + b0;
     s.chunk_lens = p.chunk_lens + b0;
+    if (TREE) s.draft_mask = p.draft_mask + (size_t)b0 * p.C_max;
     s.out = p.out + (size_t)b0 * p.C_max * p.Hq * D;
     s.lse = p.lse + (size_t)b0 * p.C_max * p.Hq;
-    hipLaunchKernelGGL((verify_attn_kernel<BF16, D>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    hipLaunchKernelGGL((verify_attn_kernel<BF16, D, TREE>), dim3(pl.P), dim3(kThreads), 0, stream, s);
   }
   if (d->ev_main_end) (void)hipEventRecord(static_cast<hipEvent_t>(d->ev_main_end), stream);
 }
 
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+// Host checks and launch of both entry points; draft_mask is NULL for a
+// chain draft.
+int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* ctx_lens,
+        const int32_t* chunk_lens, const uint64_t* draft_mask, bool tree, float scale, float* out, float* lse,
+        void* stream, const specmoe_verify_desc* desc) {
+  const int st = validate_desc(desc);
+  if (st != SPECMOE_OK) return st;
+  if (tree && desc->C_max > kMaxDraftBits) return SPECMOE_ERR_MASK;
+  if (desc->B == 0) return SPECMOE_OK;   // nothing to read or write
+  if (!q || !k_cache || !v_cache || !ctx_lens || !chunk_lens || !out || !lse) return SPECMOE_ERR_NULL_POINTER;
+  if (tree && !draft_mask) return SPECMOE_ERR_NULL_POINTER;
+  if (!isfinite(scale)) return SPECMOE_ERR_SCALE;
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return SPECMOE_ERR_ALIGN;
+  if (tree && (reinterpret_cast<uintptr_t>(draft_mask) & 7u) != 0) return SPECMOE_ERR_ALIGN;
+  const Plan pl = make_plan(desc);
+  if (!desc->workspace) return SPECMOE_ERR_NULL_POINTER;
+  if (!aligned16(desc->workspace)) return SPECMOE_ERR_ALIGN;
+  if (desc->workspace_bytes < pl.ws_bytes) return SPECMOE_ERR_WORKSPACE;
+
+  Params p;
+  p.q = static_cast<const char*>(q);
+  p.k = static_cast<const char*>(k_cache);
+  p.v = static_cast<const char*>(v_cache);
+  p.ctx_lens = ctx_lens;
+  p.chunk_lens = chunk_lens;
+  p.out = out;
+  p.lse = lse;
+  p.draft_mask = draft_mask;
+  char* ws = static_cast<char*>(desc->workspace);
+  p.counters = reinterpret_cast<int*>(ws);
+  p.ws_lse = reinterpret_cast<float*>(ws + pl.ws_lse_off);
+  p.ws_o = reinterpret_cast<float*>(ws + pl.ws_o_off);
+  p.ws_lse_bytes = (int)(pl.ws_o_off - pl.ws_lse_off);
+  p.ws_o_bytes = (int)(pl.ws_bytes - pl.ws_o_off);
+  p.B = desc->B;
+  p.Hq = desc->Hq;
+  p.Hkv = desc->Hkv;
+  p.g = pl.g;
+  p.C_max = desc->C_max;
+  p.S_max = desc->S_max;
+  p.Rcap = pl.Rcap;
+  p.P = pl.P;
+  p.sl2 = scale * kLog2e;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();  // clear a stale error from unrelated work
+  const bool bf16 = desc->dtype == SPECMOE_BF16;
+  if (tree) {
+    if (bf16 && desc->D == 128) launch<true, 128, true>(p, pl, s, desc);
+    else if (bf16) launch<true, 64, true>(p, pl, s, desc);
+    else if (desc->D == 128) launch<false, 128, true>(p, pl, s, desc);
+    else launch<false, 64, true>(p, pl, s, desc);
+  } else {
+    if (bf16 && desc->D == 128) launch<true, 128, false>(p, pl, s, desc);
+    else if (bf16) launch<true, 64, false>(p, pl, s, desc);
+    else if (desc->D == 128) launch<false, 128, false>(p, pl, s, desc);
+    else launch<false, 64, false>(p, pl, s, desc);
+  }
+  if (hipGetLastError() != hipSuccess) return SPECMOE_ERR_LAUNCH;
+  return SPECMOE_OK;
+}
 
 }  // namespace
 
@@ -1261,6 +1355,7 @@ const char* specmoe_status_str(int status) {
     case SPECMOE_ERR_ALIGN: return "q, k_cache, v_cache, out and workspace must be 16-byte aligned";
     case SPECMOE_ERR_SCALE: return "scale is not finite";
     case SPECMOE_ERR_LAUNCH: return "HIP kernel launch failed";
+    case SPECMOE_ERR_MASK: return "draft masks hold at most 64 draft tokens: C_max must be <= 64";
     default: return "unknown status";
   }
 }
@@ -1268,50 +1363,13 @@ const char* specmoe_status_str(int status) {
 int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache, const int32_t* ctx_lens,
                         const int32_t* chunk_lens, float scale, float* out, float* lse, void* stream,
                         const specmoe_verify_desc* desc) {
-  const int st = validate_desc(desc);
-  if (st != SPECMOE_OK) return st;
-  if (desc->B == 0) return SPECMOE_OK;   // nothing to read or write
-  if (!q || !k_cache || !v_cache || !ctx_lens || !chunk_lens || !out || !lse) return SPECMOE_ERR_NULL_POINTER;
-  if (!isfinite(scale)) return SPECMOE_ERR_SCALE;
-  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return SPECMOE_ERR_ALIGN;
-  const Plan pl = make_plan(desc);
-  if (!desc->workspace) return SPECMOE_ERR_NULL_POINTER;
-  if (!aligned16(desc->workspace)) return SPECMOE_ERR_ALIGN;
-  if (desc->workspace_bytes < pl.ws_bytes) return SPECMOE_ERR_WORKSPACE;
+  return run(q, k_cache, v_cache, ctx_lens, chunk_lens, nullptr, false, scale, out, lse, stream, desc);
+}
 
-  Params p;
-  p.q = static_cast<const char*>(q);
-  p.k = static_cast<const char*>(k_cache);
-  p.v = static_cast<const char*>(v_cache);
-  p.ctx_lens = ctx_lens;
-  p.chunk_lens = chunk_lens;
-  p.out = out;
-  p.lse = lse;
-  char* ws = static_cast<char*>(desc->workspace);
-  p.counters = reinterpret_cast<int*>(ws);
-  p.ws_lse = reinterpret_cast<float*>(ws + pl.ws_lse_off);
-  p.ws_o = reinterpret_cast<float*>(ws + pl.ws_o_off);
-  p.ws_lse_bytes = (int)(pl.ws_o_off - pl.ws_lse_off);
-  p.ws_o_bytes = (int)(pl.ws_bytes - pl.ws_o_off);
-  p.B = desc->B;
-  p.Hq = desc->Hq;
-  p.Hkv = desc->Hkv;
-  p.g = pl.g;
-  p.C_max = desc->C_max;
-  p.S_max = desc->S_max;
-  p.Rcap = pl.Rcap;
-  p.P = pl.P;
-  p.sl2 = scale * kLog2e;
-
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();  // clear a stale error from unrelated work
-  const bool bf16 = desc->dtype == SPECMOE_BF16;
-  if (bf16 && desc->D == 128) launch<true, 128>(p, pl, s, desc);
-  else if (bf16) launch<true, 64>(p, pl, s, desc);
-  else if (desc->D == 128) launch<false, 128>(p, pl, s, desc);
-  else launch<false, 64>(p, pl, s, desc);
-  if (hipGetLastError() != hipSuccess) return SPECMOE_ERR_LAUNCH;
-  return SPECMOE_OK;
+int specmoe_verify_attn_tree(const void* q, const void* k_cache, const void* v_cache, const int32_t* ctx_lens,
+                             const int32_t* chunk_lens, const uint64_t* draft_mask, float scale, float* out,
+                             float* lse, void* stream, const specmoe_verify_desc* desc) {
+  return run(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, true, scale, out, lse, stream, desc);
 }
 
 }  // extern "C"

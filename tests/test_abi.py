@@ -89,6 +89,42 @@ def test_null_and_alignment_and_scale(lib):
     assert _call(lib, d, scale=float("inf")) == -10
 
 
+def _call_tree(lib, desc, mask=FAKE, **kw):
+    args = dict(q=FAKE, k=FAKE, v=FAKE, ctx=FAKE, chunk=FAKE, scale=0.088, out=FAKE, lse=FAKE)
+    args.update(kw)
+    return lib.specmoe_verify_attn_tree(args["q"], args["k"], args["v"], args["ctx"], args["chunk"], mask,
+                                        args["scale"], args["out"], args["lse"], None,
+                                        ctypes.byref(desc) if desc is not None else None)
+
+
+def test_tree_entry_point_host_checks(lib):
+    d = _desc(C_max=16, Hq=32, Hkv=4)           # 128 rows, 16 draft tokens
+    d.workspace, d.workspace_bytes = FAKE, 1 << 30
+    assert _call_tree(lib, None) == -1
+    assert _call_tree(lib, d, mask=None) == -1
+    for arg in ("q", "k", "v", "ctx", "chunk", "out", "lse"):
+        assert _call_tree(lib, d, **{arg: None}) == -1, arg
+    assert _call_tree(lib, d, mask=FAKE + 4) == -9          # words are 8-byte aligned
+    assert _call_tree(lib, d, q=FAKE + 4) == -9
+    assert _call_tree(lib, d, scale=float("nan")) == -10
+    # one 64-bit word per draft token: at most 64 draft tokens
+    wide = _desc(C_max=65, Hq=1, Hkv=1, S_max=2304)
+    wide.workspace, wide.workspace_bytes = FAKE, 1 << 30
+    assert _call_tree(lib, wide) == -13
+    # the chain entry point has no such limit: with a too-small workspace it
+    # gets as far as the workspace check (and launches nothing)
+    wide.workspace_bytes = 1
+    assert _call(lib, wide) == -8
+    wide.B = 0
+    assert _call_tree(lib, wide) == -13                     # a descriptor error even for B = 0
+    # B = 0 with a valid descriptor: no pointer is looked at
+    empty = _desc(B=0, C_max=16, Hq=32, Hkv=4)
+    assert _call_tree(lib, empty, mask=None, q=None, out=None) == 0
+    # descriptor errors come first, as in the chain entry point
+    assert _call_tree(lib, _desc(D=96)) == -4
+    assert lib.specmoe_status_str(-13).decode().startswith("draft masks")
+
+
 def test_workspace_contract(lib):
     d = _desc(B=64, grid_blocks=256)
     need = lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d))
