@@ -17,6 +17,10 @@ Mixtral-8x7B (Section 6.1, dataset table): those datasets and model weights are
 not used; lengths are drawn from distributions that cover their prefix lengths
 (APPS mean 566 input tokens plus up to 1024 generated; CNN/DM mean 1006), and
 Mixtral's attention shape (32 query heads, 8 KV heads, head_dim 128) is used.
+The draft-side workload is the decode attention of the draft model's single
+layer, one new token per sequence (chunk 1): its KV cache is 1/8 of the
+target's 32 layers (Section 5.2: 17.75 GB against 142 GB), i.e. four times a
+target layer's, which is 32 KV heads of head_dim 128 (multi-head, g = 1).
 
 Recipe (all draws with numpy's PCG64 ``default_rng``):
   * lengths: ``default_rng(seed)``; context lengths first, then chunk lengths.
@@ -118,6 +122,10 @@ WORKLOADS = [
              ctx=("uniform", 512, 2048), chunk=("fixed", 16), draft="tree",
              description="Mixtral-8x7B attention shape with 16-token tree drafts, bf16: B=64, Hq=32, "
                          "Hkv=8, D=128, ctx U[512,2048], chunk 16, random recursive trees"),
+    Workload("eagle_draft_b64", 7, B=64, Hq=32, Hkv=32, D=128, dtype="bf16",
+             ctx=("uniform", 512, 2048), chunk=("fixed", 1),
+             description="draft-model decode attention (one MHA layer of the EAGLE draft for Mixtral-8x7B), "
+                         "bf16: B=64, Hq=Hkv=32, D=128, ctx U[512,2048], chunk 1"),
 ]
 BY_NAME = {w.name: w for w in WORKLOADS}
 

@@ -93,7 +93,8 @@ def test_tiny_fp32_full():
         check_case(inp, w.dtype, w.name, grid_blocks=P)
 
 
-@pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128"])
+@pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128",
+                                  "eagle_draft_b64"])
 def test_workload_reduced_batch(name):
     """Every row of a few sequences drawn from each workload's distribution."""
     w = wl.get(name)
@@ -122,7 +123,8 @@ def _full_size_inputs(w, sample):
     return host, to_dev(host["q"], "bf16"), k, v, ctx, chunk
 
 
-@pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128"])
+@pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128",
+                                  "eagle_draft_b64"])
 def test_workload_full_size_sampled(name):
     """Full-size workload in the benchmark's launch configuration (default
     grid); the oracle checks sampled sequences, every output row is
