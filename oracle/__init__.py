@@ -5,3 +5,4 @@ the benchmark's CPU-baseline leg may use it.  See ``oracle.reference``.
 """
 from .reference import (bf16_bits_to_f64, chain_mask, chunked_attention,  # noqa: F401
                         to_f64, tree_mask, verify_attn_ref)
+from .acceptance import accept_greedy_ref  # noqa: F401

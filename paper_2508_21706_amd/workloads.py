@@ -272,6 +272,68 @@ def random_draft_masks(rng: np.random.Generator, chunk_lens, C_max: int, density
     return words
 
 
+@dataclasses.dataclass(frozen=True)
+class AcceptWorkload:
+    """Inputs of the acceptance step: target logits for every chunk position
+    and the chunk's token ids."""
+    name: str
+    index: int            # RNG seed
+    B: int
+    C_max: int            # chunk length (fixed)
+    V: int                # vocabulary size
+    dtype: str            # "f32" or "bf16" logits
+    accept_prob: float    # chance that a draft token equals the planted prediction
+    description: str
+
+    @property
+    def elt_bytes(self) -> int:
+        return 4 if self.dtype == "f32" else 2
+
+
+ACCEPT_WORKLOADS = [
+    AcceptWorkload("accept_mixtral_b64", 11, B=64, C_max=5, V=32000, dtype="bf16", accept_prob=0.7,
+                   description="greedy acceptance after the Mixtral B=64 verification: chunk 5, "
+                               "vocabulary 32000, bf16 logits"),
+    AcceptWorkload("accept_large_b256", 12, B=256, C_max=8, V=32000, dtype="bf16", accept_prob=0.7,
+                   description="greedy acceptance after the B=256 verification: chunk 8, vocabulary 32000, "
+                               "bf16 logits"),
+    AcceptWorkload("accept_tiny_f32", 13, B=3, C_max=4, V=1000, dtype="f32", accept_prob=0.6,
+                   description="tiny f32 acceptance: B=3, chunk 4, vocabulary 1000"),
+]
+ACCEPT_BY_NAME = {w.name: w for w in ACCEPT_WORKLOADS}
+
+
+def make_accept_inputs(w: AcceptWorkload, chunk_lens=None, ctx_lens=None, fill: float = float("nan")):
+    """Logits [B, C_max, V], chunk token ids [B, C_max] (int32), ctx_lens and
+    chunk_lens (int32 [B]) of an acceptance workload.
+
+    Recipe (``default_rng([seed, 4])``): logits N(0, 1); in each valid row i
+    a planted token p_i (uniform) gets the value 8 -- far above the N(0, 1)
+    draws, so it is almost surely the row's maximum, though nothing relies on
+    that.  Chunk token 0 is uniform; chunk token i + 1 is p_i with probability
+    ``accept_prob``, else a uniform token other than p_i.  Context lengths are
+    U[512, 2048] unless given; chunk lengths default to C_max.  Rows past c_b
+    hold ``fill`` (logits) and -1 (tokens).
+    """
+    rng = np.random.default_rng([w.index, 4])
+    B, C, V = w.B, w.C_max, w.V
+    chunk = np.full(B, C, np.int32) if chunk_lens is None else np.asarray(chunk_lens, np.int32)
+    ctx = rng.integers(512, 2049, size=B).astype(np.int32) if ctx_lens is None else np.asarray(ctx_lens, np.int32)
+    x = rng.standard_normal((B, C, V), dtype=np.float32)
+    planted = rng.integers(0, V, size=(B, C))
+    x[np.arange(B)[:, None], np.arange(C)[None, :], planted] = 8.0
+    tokens = np.full((B, C), -1, np.int32)
+    tokens[:, 0] = rng.integers(0, V, size=B)
+    hit = rng.random((B, C)) < w.accept_prob
+    other = (planted + rng.integers(1, V, size=(B, C))) % V
+    tokens[:, 1:] = np.where(hit[:, :-1], planted[:, :-1], other[:, :-1])
+    for b in range(B):
+        x[b, chunk[b]:] = fill
+        tokens[b, chunk[b]:] = -1
+    logits = _encode(x, w.dtype)
+    return dict(logits=logits, tokens=tokens, ctx_lens=ctx, chunk_lens=chunk, planted=planted, workload=w)
+
+
 def algorithmic_kv_bytes(w: Workload, ctx_lens, chunk_lens) -> int:
     """K+V bytes of valid rows: sum_b Hkv * (l_b + c_b) * D * elt * 2.
 
