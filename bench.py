@@ -6,6 +6,10 @@ workload, with every input already resident in HBM.  Prints ONE JSON line on std
 
     python bench.py [--steps K] [--warmup W] [--workload mixtral_b64]
 
+The acceptance step that follows verification has workloads of its own
+(``--workload accept_mixtral_b64`` etc.): one step is one greedy-acceptance
+call over the batch's logits, and value = logits GB/s.
+
 value = effective KV GB/s = sum_b Hkv*(l_b + c_b)*D*elt*2 / t_step, the K+V
 bytes of every valid row (the attention row of the paper's cost table,
 2*b*s*h/g elements, Section 3.2).  Input sets are rotated so that successive
@@ -33,28 +37,130 @@ METRIC = "effective KV HBM GB/s and verified draft tokens/sec, Mixtral shape B=6
 HBM_PEAK_GBS = 8000.0
 MAIN_KERNEL = "verify_attn_kernel"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2508_21706_amd", "csrc", "verify_attn.hip")
+ACCEPT_METRIC = "acceptance step: logits HBM GB/s and accepted-token decisions per second"
+ACCEPT_KERNEL = "accept_kernel"
+ACCEPT_SOURCE = os.path.join(ROOT, "paper_2508_21706_amd", "csrc", "accept.hip")
 
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def source_digest() -> str:
-    with open(KERNEL_SOURCE, "rb") as f:
+def source_digest(path: str = KERNEL_SOURCE) -> str:
+    with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def load_traffic(workload: str):
-    """HBM bytes per launch of the main kernel from the committed rocprofv3
-    counter summary, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"{MAIN_KERNEL}_{workload}_traffic.txt")
+def load_traffic(workload: str, kernel: str = MAIN_KERNEL, source: str = KERNEL_SOURCE):
+    """HBM bytes per launch of a kernel from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_source_sha256_16") != source_digest():
+    if rec.get("kernel_source_sha256_16") != source_digest(source):
         return None
     return rec.get("hbm_bytes_per_launch")
+
+
+def run_timed(step, args, stream):
+    """Settle, warm up, then time exactly args.steps steps between two
+    synchronisations; returns (ms per step, settle steps)."""
+    import torch
+    settle_steps = 0
+    torch.cuda.synchronize()
+    t_settle = time.time()
+    while (time.time() - t_settle) * 1e3 < args.settle_ms:
+        for _ in range(20):
+            step(settle_steps)
+            settle_steps += 1
+        torch.cuda.synchronize()
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    return t_start.elapsed_time(t_end) / args.steps, settle_steps
+
+
+def bench_accept(args):
+    """The acceptance step: one greedy-acceptance launch per step over the
+    batch's logits (rotated over enough copies that they come from HBM)."""
+    import torch
+    import paper_2508_21706_amd as pkg
+    from paper_2508_21706_amd import workloads as wl
+
+    w = wl.ACCEPT_BY_NAME[args.workload]
+    dev = torch.device("cuda:0")
+    inp = wl.make_accept_inputs(w)
+    chunk = inp["chunk_lens"]
+    rows = int(chunk.sum())
+    logit_bytes = rows * w.V * w.elt_bytes
+    # algorithmic bytes per launch: the valid logits rows, the chunk tokens and
+    # lengths read, and the argmax / accepted / next / new-length outputs
+    launch_bytes = logit_bytes + rows * 4 + w.B * 8 + w.B * w.C_max * 4 + w.B * 12
+    if w.dtype == "bf16":
+        x = torch.from_numpy(inp["logits"].view(np.int16)).view(torch.bfloat16).to(dev)
+    else:
+        x = torch.from_numpy(inp["logits"]).to(dev)
+    n_sets = args.rotate or max(4, int(np.ceil(1.0e9 / x.numel() / x.element_size())))
+    sets = [x] + [x.clone() for _ in range(n_sets - 1)]
+    tokens = torch.from_numpy(inp["tokens"]).to(dev)
+    ctx = torch.from_numpy(inp["ctx_lens"]).to(dev)
+    chunk_d = torch.from_numpy(chunk).to(dev)
+    desc = pkg.accept_desc(w.B, w.C_max, w.V, pkg.binding.SPECMOE_BF16 if w.dtype == "bf16" else 0)
+    ws = pkg.alloc_accept_workspace(desc, dev)
+    out = {"argmax": torch.empty((w.B, w.C_max), dtype=torch.int32, device=dev),
+           "accepted": torch.empty((w.B,), dtype=torch.int32, device=dev),
+           "next_token": torch.empty((w.B,), dtype=torch.int32, device=dev),
+           "new_ctx_lens": torch.empty((w.B,), dtype=torch.int32, device=dev)}
+    stream = torch.cuda.current_stream(dev)
+    log(f"{n_sets} logits sets x {logit_bytes / 1e6:.1f} MB, {w.B} sequences x chunk {w.C_max}, vocabulary {w.V}")
+
+    def step(i):
+        pkg.accept_greedy(sets[i % n_sets], tokens, ctx, chunk_d, out=out, workspace=ws, stream=stream)
+
+    ms, settle_steps = run_timed(step, args, stream)
+    t = ms / 1e3
+    value = logit_bytes / t / 1e9
+    achieved = launch_bytes / t / 1e9
+    log(f"step {ms * 1e3:.2f} us -> {value:.0f} GB/s of logits, {w.B / t / 1e6:.2f} M sequence decisions/s")
+    cpu = None
+    if args.cpu_budget > 0:
+        from oracle import accept_greedy_ref
+        log("timing the oracle on the host ...")
+        passes, t_total = 0, 0.0
+        while t_total < args.cpu_budget:
+            t0 = time.perf_counter()
+            accept_greedy_ref(inp["logits"], inp["tokens"], inp["ctx_lens"], chunk, w.dtype)
+            t_total += time.perf_counter() - t0
+            passes += 1
+        cpu = {"value": passes * logit_bytes / t_total / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"{passes} passes over the whole batch ({w.B} sequences, {rows} logits rows), numpy "
+                         f"oracle, {t_total:.1f} s"}
+    traffic = load_traffic(w.name, ACCEPT_KERNEL, ACCEPT_SOURCE)
+    rec = {
+        "metric": ACCEPT_METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "settle_steps": settle_steps, "ms_per_step": round(ms, 6),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "description": w.description, "B": w.B, "C_max": w.C_max, "V": w.V,
+                   "input_sets": n_sets, "parallelism": "single GPU"},
+        "sequence_decisions_per_s": round(w.B / t, 1),
+        "roofline": {"bound": "hbm", "kernel": ACCEPT_KERNEL, "achieved": round(achieved, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "traffic_unit": "HBM bytes per launch",
+                     "traffic_over_algorithmic": round(traffic / launch_bytes, 4) if traffic else None,
+                     "algorithmic_bytes_per_launch": launch_bytes, "avg_launch_us": round(t * 1e6, 3)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
 
 
 def cpu_baseline(inp, w, budget_s: float):
@@ -129,6 +235,9 @@ def main():
     import paper_2508_21706_amd as pkg
     from paper_2508_21706_amd import workloads as wl
 
+    if args.workload in wl.ACCEPT_BY_NAME:
+        bench_accept(args)
+        return
     w = wl.get(args.workload)
     dev = torch.device("cuda:0")
     t0 = time.time()
@@ -175,30 +284,10 @@ def main():
             pkg.verify_attn(q, k, v, ctx_d, chunk_d, w.scale, out=out, lse=lse, workspace=ws,
                             grid_blocks=args.grid_blocks, stream=stream, events=events)
 
-    # settle: sustained load until the GPU runs at its working clock (a short
-    # warmup alone measures the ramp: about 5% slower on this workload)
-    settle_steps = 0
-    torch.cuda.synchronize()
-    t_settle = time.time()
-    while (time.time() - t_settle) * 1e3 < args.settle_ms:
-        for _ in range(20):
-            step(settle_steps)
-            settle_steps += 1
-        torch.cuda.synchronize()
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-
-    # timed region: exactly K steps, bracketed by synchronisations
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(i)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    # settle (sustained load until the GPU runs at its working clock: a short
+    # warmup alone measures the ramp, about 5% slower on this workload), warm
+    # up, then the timed region: exactly K steps, bracketed by synchronisations
+    ms_per_step, settle_steps = run_timed(step, args, stream)
 
     # Average launch duration of the main kernel: every step is one launch of
     # it on `stream`, so the timed region's HIP events divided by K give it

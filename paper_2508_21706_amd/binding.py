@@ -38,6 +38,15 @@ class Desc(ctypes.Structure):
     ]
 
 
+class AcceptDesc(ctypes.Structure):
+    """Mirror of ``specmoe_accept_desc``."""
+    _fields_ = [
+        ("B", ctypes.c_int32), ("C_max", ctypes.c_int32), ("V", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("split", ctypes.c_int32), ("flags", ctypes.c_int32),
+        ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+    ]
+
+
 class SpecMoEError(RuntimeError):
     def __init__(self, status: int, text: str):
         super().__init__(f"{STATUS.get(status, status)}: {text}")
@@ -72,6 +81,13 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
                                                        ctypes.POINTER(Desc)]
     lib.specmoe_verify_attn_key_tile.restype = ctypes.c_int32
     lib.specmoe_verify_attn_key_tile.argtypes = [ctypes.POINTER(Desc)]
+    lib.specmoe_accept_greedy.restype = ctypes.c_int
+    lib.specmoe_accept_greedy.argtypes = [ctypes.c_void_p] * 9 + [ctypes.POINTER(AcceptDesc)]
+    lib.specmoe_accept_workspace_bytes.restype = ctypes.c_size_t
+    lib.specmoe_accept_workspace_bytes.argtypes = [ctypes.POINTER(AcceptDesc)]
+    lib.specmoe_accept_workspace_init.restype = ctypes.c_int
+    lib.specmoe_accept_workspace_init.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                                  ctypes.POINTER(AcceptDesc)]
     lib.specmoe_status_str.restype = ctypes.c_char_p
     lib.specmoe_status_str.argtypes = [ctypes.c_int]
     if path is None:
@@ -228,3 +244,71 @@ def _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse
     if st != 0:
         raise SpecMoEError(st, status_str(st))
     return out, lse
+
+
+# ------------------------------------------------------------ acceptance step
+
+def accept_desc(B, C_max, V, dtype: int, split: int = 0) -> AcceptDesc:
+    return AcceptDesc(B, C_max, V, dtype, split, 0, None, 0)
+
+
+def alloc_accept_workspace(desc: AcceptDesc, device, stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Allocate a workspace for ``desc`` and zero its counters on the stream."""
+    lib = load_library()
+    n = int(lib.specmoe_accept_workspace_bytes(ctypes.byref(desc)))
+    if n == 0:
+        raise SpecMoEError(-2, "invalid acceptance descriptor")
+    ws = torch.empty(n, dtype=torch.uint8, device=device)
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    st = lib.specmoe_accept_workspace_init(ws.data_ptr(), n, s.cuda_stream, ctypes.byref(desc))
+    if st != 0:
+        raise SpecMoEError(st, status_str(st))
+    return ws
+
+
+def accept_greedy(logits: torch.Tensor, tokens: torch.Tensor, ctx_lens: torch.Tensor, chunk_lens: torch.Tensor,
+                  out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None, split: int = 0,
+                  stream: Optional[torch.cuda.Stream] = None, in_place: bool = False):
+    """Greedy acceptance after verification; see ``include/specmoe_accept.h``.
+
+    logits [B, C_max, V] (bf16 or f32), tokens int32 [B, C_max], ctx_lens /
+    chunk_lens int32 [B], all on the GPU.  Returns a dict of int32 tensors:
+    argmax [B, C_max], accepted [B], next_token [B], new_ctx_lens [B] (with
+    ``in_place``, ctx_lens itself is updated and returned as new_ctx_lens).
+    ``out`` may supply those tensors.
+    """
+    lib = load_library()
+    if logits.dim() != 3:
+        raise ValueError("logits must be [B, C_max, V]")
+    B, C_max, V = logits.shape
+    _check(logits, "logits", (B, C_max, V), logits.dtype)
+    _check(tokens, "tokens", (B, C_max), torch.int32)
+    _check(ctx_lens, "ctx_lens", (B,), torch.int32)
+    _check(chunk_lens, "chunk_lens", (B,), torch.int32)
+    dev = logits.device
+    if out is None:
+        out = {"argmax": torch.empty((B, C_max), dtype=torch.int32, device=dev),
+               "accepted": torch.empty((B,), dtype=torch.int32, device=dev),
+               "next_token": torch.empty((B,), dtype=torch.int32, device=dev)}
+        if not in_place:
+            out["new_ctx_lens"] = torch.empty((B,), dtype=torch.int32, device=dev)
+    if in_place:
+        out["new_ctx_lens"] = ctx_lens
+    _check(out["argmax"], "argmax", (B, C_max), torch.int32)
+    for k in ("accepted", "next_token", "new_ctx_lens"):
+        _check(out[k], k, (B,), torch.int32)
+    desc = accept_desc(B, C_max, V, _dtype_code(logits), split)
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    if B == 0:
+        return out
+    if workspace is None:
+        workspace = alloc_accept_workspace(desc, dev, s)
+    desc.workspace = workspace.data_ptr()
+    desc.workspace_bytes = workspace.numel() * workspace.element_size()
+    st = lib.specmoe_accept_greedy(logits.data_ptr(), tokens.data_ptr(), ctx_lens.data_ptr(), chunk_lens.data_ptr(),
+                                   out["argmax"].data_ptr(), out["accepted"].data_ptr(),
+                                   out["next_token"].data_ptr(), out["new_ctx_lens"].data_ptr(), s.cuda_stream,
+                                   ctypes.byref(desc))
+    if st != 0:
+        raise SpecMoEError(st, status_str(st))
+    return out

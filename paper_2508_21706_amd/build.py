@@ -12,7 +12,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SOURCES = [os.path.join(HERE, "csrc", "verify_attn.hip")]
+SOURCES = [os.path.join(HERE, "csrc", "verify_attn.hip"), os.path.join(HERE, "csrc", "accept.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 OUTPUT = os.path.join(HERE, "libspecmoe_verify.so")
 ARCH = "gfx950"

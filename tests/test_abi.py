@@ -11,6 +11,8 @@ from paper_2508_21706_amd import binding as bd
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "specmoe_verify.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if h.endswith(".h")]
 
 FAKE = 0x10000          # 16-byte aligned, never dereferenced by these tests
 
@@ -21,14 +23,15 @@ def lib():
 
 
 def header_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(specmoe_\w+)\s*\(", text)))
 
 
 def test_exports_every_declared_function(lib):
     names = header_functions()
-    assert {"specmoe_verify_attn", "specmoe_verify_attn_workspace_bytes",
+    assert {"specmoe_verify_attn", "specmoe_verify_attn_workspace_bytes", "specmoe_verify_attn_tree",
+            "specmoe_accept_greedy", "specmoe_accept_workspace_bytes", "specmoe_accept_workspace_init",
             "specmoe_status_str"} <= set(names)
     for n in names:
         assert hasattr(lib, n), f"{n} is declared in the header but not exported"
@@ -164,3 +167,62 @@ def test_empty_batch_is_a_no_op(lib):
     assert _call(lib, _desc(B=0)) == 0
     assert _call(lib, _desc(B=0), q=None, k=None, v=None, ctx=None, chunk=None, out=None, lse=None) == 0
     assert _call(lib, _desc(B=0, dtype=9)) == -5    # the descriptor is still validated
+
+
+# ------------------------------------------------------------ acceptance step
+
+def _adesc(**kw):
+    base = dict(B=4, C_max=5, V=32000, dtype=bd.SPECMOE_BF16, split=0)
+    base.update(kw)
+    return bd.accept_desc(**base)
+
+
+def _acall(lib, desc, logits=FAKE, tokens=FAKE, ctx=FAKE, chunk=FAKE, am=FAKE, acc=FAKE, nxt=FAKE, new=FAKE):
+    return lib.specmoe_accept_greedy(logits, tokens, ctx, chunk, am, acc, nxt, new, None,
+                                     ctypes.byref(desc) if desc is not None else None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dtype=3), -5),
+    (dict(B=-1), -2),
+    (dict(B=65537), -2),
+    (dict(C_max=0), -2),
+    (dict(C_max=1025), -2),
+    (dict(V=0), -2),
+    (dict(V=32001), -2),                          # rows are read in 16-byte vectors
+    (dict(V=1002, dtype=bd.SPECMOE_F32), -2),
+    (dict(split=1000), -2),
+    (dict(split=-2048), -2),
+    (dict(B=4096, C_max=1024, V=32000), -2),      # element offsets would pass 2^31
+])
+def test_accept_invalid_descriptor(lib, kw, code):
+    assert _acall(lib, _adesc(**kw)) == code
+    assert lib.specmoe_accept_workspace_bytes(ctypes.byref(_adesc(**kw))) == 0
+
+
+def test_accept_host_checks_and_workspace(lib):
+    d = _adesc()
+    need = lib.specmoe_accept_workspace_bytes(ctypes.byref(d))
+    items = (32000 + 4095) // 4096                # default: 8 KB of bf16 logits per item
+    assert need == 65536 * 4 + 4 * 5 * items * 8
+    d32 = _adesc(dtype=bd.SPECMOE_F32, V=32000)
+    assert lib.specmoe_accept_workspace_bytes(ctypes.byref(d32)) == 65536 * 4 + 4 * 5 * 16 * 8
+    assert lib.specmoe_accept_workspace_bytes(ctypes.byref(_adesc(split=1024))) == 65536 * 4 + 4 * 5 * 32 * 8
+    assert _acall(lib, None) == -1
+    d.flags = 1
+    assert _acall(lib, d) == -12
+    d.flags = 0
+    assert _acall(lib, d) == -1                   # workspace needed but NULL
+    d.workspace, d.workspace_bytes = FAKE, need - 1
+    assert _acall(lib, d) == -8
+    d.workspace, d.workspace_bytes = FAKE + 8, need
+    assert _acall(lib, d) == -9
+    d.workspace = FAKE
+    for arg in ("logits", "tokens", "ctx", "chunk", "am", "acc", "nxt", "new"):
+        assert _acall(lib, d, **{arg: None}) == -1, arg
+    assert _acall(lib, d, logits=FAKE + 4) == -9
+    assert _acall(lib, _adesc(B=0), logits=None, tokens=None) == 0
+    init = lib.specmoe_accept_workspace_init
+    assert init(None, need, None, ctypes.byref(_adesc())) == -1
+    assert init(FAKE, need - 1, None, ctypes.byref(_adesc())) == -8
+    assert init(FAKE + 4, need, None, ctypes.byref(_adesc())) == -9
