@@ -65,10 +65,19 @@ def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
     return as_f32.astype(np.float64)
 
 
+def f16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """Decode IEEE binary16 values stored as uint16 bit patterns into float64
+    (exact: every binary16 value is a float64 value)."""
+    return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+
+
 def to_f64(x: np.ndarray, dtype: str) -> np.ndarray:
-    """Input values as float64: ``dtype`` is "bf16" (uint16 bits) or "f32"."""
+    """Input values as float64: ``dtype`` is "bf16" or "f16" (uint16 bits) or
+    "f32"."""
     if dtype == "bf16":
         return bf16_bits_to_f64(x)
+    if dtype == "f16":
+        return f16_bits_to_f64(x)
     if dtype == "f32":
         return np.asarray(x, dtype=np.float32).astype(np.float64)
     raise ValueError(f"unknown dtype {dtype!r}")
@@ -133,7 +142,7 @@ def verify_attn_ref(q, k_cache, v_cache, ctx_lens, chunk_lens, scale: float,
     k_cache  [B, Hkv, S_max, D]     rows [0, l_b) cached context, rows
     v_cache  [B, Hkv, S_max, D]     [l_b, l_b + c_b) the chunk's own K/V
     ctx_lens, chunk_lens  [B]       l_b and c_b
-    dtype    "bf16" (uint16 bit patterns) or "f32"
+    dtype    "bf16" or "f16" (uint16 bit patterns) or "f32"
     units    optional iterable of (b, kv_head) pairs to compute; the others
              are left NaN (for sampled checks of large workloads)
     draft_mask  optional integer array [B, C_max] of draft-mask words (see

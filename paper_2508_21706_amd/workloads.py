@@ -31,8 +31,8 @@ Recipe (all draws with numpy's PCG64 ``default_rng``):
     shape [Hkv, T_b, D] written to rows [0, T_b); v likewise with
     ``[seed, 2, b]``.  Each sequence's slab can therefore be regenerated on its
     own, which lets a test check sampled sequences of a large workload.
-  * bf16 workloads round each float32 value once, to nearest-even, to bf16; the
-    same bits feed the GPU and the oracle.
+  * bf16 (f16) workloads round each float32 value once, to nearest-even, to
+    bf16 (binary16); the same bits feed the GPU and the oracle.
   * Rows that hold no valid data (cache rows >= T_b, query rows >= c_b) are
     filled with ``fill`` (NaN by default) so that any read of them shows up.
   * Tree drafts (workloads with ``draft="tree"``): the draft tokens of
@@ -52,6 +52,7 @@ from typing import Optional, Sequence
 import numpy as np
 
 BF16_NAN = np.uint16(0x7FC0)
+F16_NAN = np.uint16(0x7E00)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -62,7 +63,7 @@ class Workload:
     Hq: int
     Hkv: int
     D: int
-    dtype: str            # "f32" or "bf16"
+    dtype: str            # "f32", "bf16" or "f16"
     ctx: tuple            # ("fixed", [..]) | ("uniform", lo, hi) | ("loguniform", lo, hi)
     chunk: tuple          # ("fixed", n) | ("uniform", lo, hi)
     description: str
@@ -122,6 +123,10 @@ WORKLOADS = [
              ctx=("uniform", 512, 2048), chunk=("fixed", 16), draft="tree",
              description="Mixtral-8x7B attention shape with 16-token tree drafts, bf16: B=64, Hq=32, "
                          "Hkv=8, D=128, ctx U[512,2048], chunk 16, random recursive trees"),
+    Workload("mixtral_f16_b64", 8, B=64, Hq=32, Hkv=8, D=128, dtype="f16",
+             ctx=("uniform", 512, 2048), chunk=("fixed", 5),
+             description="Mixtral-8x7B attention shape with an FP16 KV cache (the paper's precision): B=64, "
+                         "Hq=32, Hkv=8, D=128, ctx U[512,2048], chunk 5"),
     Workload("eagle_draft_b64", 7, B=64, Hq=32, Hkv=32, D=128, dtype="bf16",
              ctx=("uniform", 512, 2048), chunk=("fixed", 1),
              description="draft-model decode attention (one MHA layer of the EAGLE draft for Mixtral-8x7B), "
@@ -132,7 +137,7 @@ BY_NAME = {w.name: w for w in WORKLOADS}
 
 def get(name_or_index) -> Workload:
     if isinstance(name_or_index, int):
-        return WORKLOADS[name_or_index - 1]
+        return next(w for w in WORKLOADS if w.index == name_or_index)
     return BY_NAME[name_or_index]
 
 
@@ -174,13 +179,25 @@ def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     return rounded
 
 
+def f32_to_f16_bits(x: np.ndarray) -> np.ndarray:
+    """Round float32 to IEEE binary16 (numpy's conversion: nearest, ties to
+    even); returns the uint16 bits.  Input preparation only."""
+    return np.ascontiguousarray(x, dtype=np.float32).astype(np.float16).view(np.uint16)
+
+
 def _encode(x: np.ndarray, dtype: str) -> np.ndarray:
-    return f32_to_bf16_bits(x) if dtype == "bf16" else np.ascontiguousarray(x, np.float32)
+    if dtype == "bf16":
+        return f32_to_bf16_bits(x)
+    if dtype == "f16":
+        return f32_to_f16_bits(x)
+    return np.ascontiguousarray(x, np.float32)
 
 
 def _fill_value(dtype: str, fill: float):
     if dtype == "bf16":
         return BF16_NAN if math.isnan(fill) else f32_to_bf16_bits(np.float32([fill]))[0]
+    if dtype == "f16":
+        return F16_NAN if math.isnan(fill) else f32_to_f16_bits(np.float32([fill]))[0]
     return np.float32(fill)
 
 
@@ -211,7 +228,7 @@ def make_inputs(w: Workload, fill: float = float("nan"),
         chunk = np.asarray(chunk_lens, dtype=np.int32)
     B, C, S = len(ctx), w.C_max, w.S_max
     fv = _fill_value(w.dtype, fill)
-    store = np.uint16 if w.dtype == "bf16" else np.float32
+    store = np.float32 if w.dtype == "f32" else np.uint16
 
     qrng = np.random.default_rng([w.index, 0])
     q = _encode(qrng.standard_normal((B, C, w.Hq, w.D), dtype=np.float32), w.dtype)

@@ -89,6 +89,30 @@ def pin_bf16_decoding(m):
     assert math.copysign(1.0, got[4]) == -1.0
 
 
+def pin_f16_decoding(m):
+    """IEEE binary16 bit patterns decode exactly (the paper's KV precision,
+    Section 3.3): normal, largest finite, subnormal, signed zero, infinity."""
+    bits = np.array([0x3C00, 0xC000, 0x4248, 0x7BFF, 0x0001, 0x0400, 0x8000, 0x7C00, 0x3555], np.uint16)
+    want = [1.0, -2.0, 3.140625, 65504.0, 2.0 ** -24, 2.0 ** -14, -0.0, math.inf, 0.333251953125]
+    got = m.to_f64(bits, "f16")
+    assert got.dtype == np.float64
+    for g, w in zip(got, want):
+        assert g == w, (g, w)
+    assert math.copysign(1.0, got[6]) == -1.0
+
+
+def pin_f16_path(m):
+    """f16 inputs give the results of the f32 values they encode."""
+    rng = np.random.default_rng(19)
+    q, k, v, ctx, chunk = _rand_case(rng)
+    qh, kh, vh = (a.astype(np.float16).view(np.uint16) for a in (q, k, v))
+    back = lambda bits: bits.view(np.float16).astype(np.float32)
+    o1, s1 = m.verify_attn_ref(qh, kh, vh, ctx, chunk, 0.3, "f16")
+    o2, s2 = m.verify_attn_ref(back(qh), back(kh), back(vh), ctx, chunk, 0.3, "f32")
+    np.testing.assert_array_equal(o1, o2)
+    np.testing.assert_array_equal(s1, s2)
+
+
 def pin_hand_example(m):
     q, k, v, ctx, chunk, out, lse = _load_hand_example()
     o, s = m.verify_attn_ref(q, k, v, ctx, chunk, 1.0, "f32")
@@ -372,7 +396,7 @@ def pin_tree_all_ones_is_bidirectional(m):
             np.testing.assert_allclose(o[b, : chunk[b], h], ref, rtol=0, atol=1e-12)
 
 
-PINS = [pin_bf16_decoding, pin_hand_example, pin_uniform_closed_form, pin_decode_is_sdpa,
+PINS = [pin_bf16_decoding, pin_f16_decoding, pin_f16_path, pin_hand_example, pin_uniform_closed_form, pin_decode_is_sdpa,
         pin_chunk_is_causal_prefill, pin_sequential_decode, pin_gqa_is_repeated_mha,
         pin_invariants, pin_one_hot, pin_padding_and_poison, pin_bf16_path,
         pin_tree_chain_words_are_causal, pin_tree_row_is_its_root_path, pin_tree_matches_sdpa_boolean_mask,
@@ -399,6 +423,7 @@ MUTATIONS = {
     "v_from_k": ("V = to_f64(v_cache[b, kvh, : l + n], dtype)",
                  "V = to_f64(k_cache[b, kvh, : l + n], dtype)"),
     "bf16_shift": ("<< np.uint32(16)", "<< np.uint32(15)"),
+    "f16_read_as_bf16": ("        return f16_bits_to_f64(x)", "        return bf16_bits_to_f64(x)"),
     "padding_lse_zero": ("lse[b, n:, h] = -np.inf", "lse[b, n:, h] = 0.0"),
     "q_wrong_token": ("Q = to_f64(q[b, :n, h], dtype)", "Q = to_f64(q[b, 1 : n + 1, h], dtype)"),
     "transposed_scores": ("out[seen] = (E / Z) @ V", "out[seen] = (E / Z) @ V[::-1]"),
