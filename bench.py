@@ -255,8 +255,9 @@ def main():
     launch_bytes = kv_bytes + int(chunk.sum()) * (w.Hq * (w.D * elt + (w.D + 1) * 4) + (8 if tree else 0))
 
     def to_dev(a):
-        if w.dtype == "bf16":
-            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        if w.dtype in ("bf16", "f16"):
+            t16 = torch.bfloat16 if w.dtype == "bf16" else torch.float16
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(t16).to(dev)
         return torch.from_numpy(a).to(dev)
 
     set_bytes = inp["k_cache"].nbytes * 2

@@ -29,10 +29,12 @@
 extern "C" {
 #endif
 
-/* Element type of q, k_cache and v_cache.  out and lse are always float32. */
+/* Element type of q, k_cache and v_cache.  out and lse are always float32.
+ * FP16 is the KV precision the paper assumes (Section 3.3, Section 6.1). */
 typedef enum {
   SPECMOE_F32 = 0,
-  SPECMOE_BF16 = 1
+  SPECMOE_BF16 = 1,
+  SPECMOE_F16 = 2
 } specmoe_dtype;
 
 /* Status codes returned by the entry points (0 = success). */

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
 
 SPECMOE_F32 = 0
 SPECMOE_BF16 = 1
+SPECMOE_F16 = 2
 
 STATUS = {
     0: "SPECMOE_OK", -1: "SPECMOE_ERR_NULL_POINTER", -2: "SPECMOE_ERR_SHAPE", -3: "SPECMOE_ERR_GQA",
@@ -113,9 +114,11 @@ def make_desc(B, Hq, Hkv, D, C_max, S_max, dtype: int, grid_blocks: int = 0, fla
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype == torch.bfloat16:
         return SPECMOE_BF16
+    if t.dtype == torch.float16:
+        return SPECMOE_F16
     if t.dtype == torch.float32:
         return SPECMOE_F32
-    raise TypeError(f"unsupported dtype {t.dtype}; expected torch.bfloat16 or torch.float32")
+    raise TypeError(f"unsupported dtype {t.dtype}; expected torch.bfloat16, torch.float16 or torch.float32")
 
 
 def desc_for(q: torch.Tensor, k_cache: torch.Tensor, grid_blocks: int = 0) -> Desc:
@@ -164,7 +167,7 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                 check_lengths: bool = False):
     """Chunked verification attention; see ``include/specmoe_verify.h``.
 
-    q [B, C_max, Hq, D], k_cache / v_cache [B, Hkv, S_max, D] (bf16 or f32),
+    q [B, C_max, Hq, D], k_cache / v_cache [B, Hkv, S_max, D] (bf16, f16 or f32),
     ctx_lens / chunk_lens int32 [B], all on the GPU.  Returns (out, lse) as
     float32 [B, C_max, Hq, D] and [B, C_max, Hq].  ``workspace`` (from
     ``alloc_workspace``) is reused across calls; without one, a fresh

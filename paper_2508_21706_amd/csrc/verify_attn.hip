@@ -45,10 +45,11 @@
 //     the B operand of O^T = V^T P^T.  A consumer wave takes two 16-key blocks
 //     of a tile; the waves that share a row block merge their partial (max,
 //     sum, O) states through LDS at the end of each unit.
-//   * bf16 inputs use v_mfma_f32_16x16x32_bf16 for the scores and for P V
-//     (one 32-key contraction over the wave's two blocks), with fp32
-//     accumulation (P is rounded to bf16 for the PV product); f32 inputs use
-//     v_mfma_f32_16x16x4_f32.
+//   * bf16 (f16) inputs use v_mfma_f32_16x16x32_bf16 (_f16) for the scores
+//     and for P V (one 32-key contraction over the wave's two blocks), with
+//     fp32 accumulation (P is rounded to the input type for the PV product);
+//     f32 inputs use v_mfma_f32_16x16x4_f32.  The two 16-bit types share
+//     every layout and differ only in these instructions.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -85,6 +86,10 @@ constexpr float kLn2 = 0.6931471805599453f;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+
+// Element types of q, k and v (the specmoe_dtype codes)
+constexpr int kF32 = SPECMOE_F32, kBF16 = SPECMOE_BF16, kF16 = SPECMOE_F16;
 typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((ext_vector_type(4))) int i32x4;
 
@@ -118,9 +123,10 @@ struct Params {
   const uint64_t* draft_mask;   // [B][C_max] draft-mask words (tree drafts only)
 };
 
-template <bool BF16, int D>
+// W16: 16-bit elements (bf16 or f16), which share every layout
+template <bool W16, int D>
 struct Cfg {
-  static constexpr int kElt = BF16 ? 2 : 4;
+  static constexpr int kElt = W16 ? 2 : 4;
   static constexpr int kRowBytes = D * kElt;
   static constexpr int kChunks = kRowBytes / 16;           // 16-byte chunks per row
   static constexpr int kTileKeys = kHalf / kRowBytes;
@@ -130,7 +136,7 @@ struct Cfg {
   // transposed V reads take 4 rows x 32 bytes per 16 lanes, which one pad
   // would leave two-way bank conflicted); other layouts keep one.
   static constexpr int kSlotsK = kChunks + 1;
-  static constexpr int kSlotsV = kChunks + (BF16 && D == 128 ? 2 : 1);
+  static constexpr int kSlotsV = kChunks + (W16 && D == 128 ? 2 : 1);
   static constexpr int kPitchK = 16 * kSlotsK;              // padded LDS row pitches
   static constexpr int kPitchV = 16 * kSlotsV;
   static constexpr int kLdsK = kTileKeys * kPitchK;         // LDS bytes of a staged K (V) tile
@@ -205,6 +211,35 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
   typedef float f32x2_t __attribute__((ext_vector_type(2)));
   return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
+}
+
+// The same for f16 (two conversions to nearest even, one pack).
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), f16x2_t));
+}
+
+// Probabilities of 8 keys packed into a 16-bit MFMA operand
+template <int ELT>
+__device__ __forceinline__ u32x4 pack_p(const float (&pr)[8]) {
+  if constexpr (ELT == kF16)
+    return u32x4{pack_f16x2(pr[0], pr[1]), pack_f16x2(pr[2], pr[3]), pack_f16x2(pr[4], pr[5]),
+                 pack_f16x2(pr[6], pr[7])};
+  else
+    return u32x4{pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]), pack_bf16x2(pr[4], pr[5]),
+                 pack_bf16x2(pr[6], pr[7])};
+}
+
+// 16x16x32 MFMA on 16-bit operands (8 elements per lane), fp32 accumulation
+template <int ELT>
+__device__ __forceinline__ f32x4 mfma32(const u32x4& a, const u32x4& b, f32x4 acc) {
+  if constexpr (ELT == kF16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b), acc,
+                                                  0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                   acc, 0, 0, 0);
 }
 
 // Lengths of sequence b, clamped into the documented ranges so that no access
@@ -399,9 +434,10 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
 
 // TREE: the draft region obeys per-token draft-mask words instead of the
 // chain mask.
-template <bool BF16, int D, bool TREE>
+template <int ELT, int D, bool TREE>
 __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
-  using C = Cfg<BF16, D>;
+  constexpr bool W16 = ELT != kF32;   // 16-bit elements
+  using C = Cfg<W16, D>;
   __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
   __shared__ uint32_t seqs[kMaxSeqs];     // packed (T, c) of every sequence of the launch
   __shared__ int pref[kMaxSeqs + 1];      // tiles per KV head of the sequences before b
@@ -889,9 +925,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         const char* krow = ks + (kb0 * kBlk + lm) * C::kPitchK + 16 * lg;
         // S^T chunk J of block h: kop(J, h) times Q chunk J
         auto score = [&](f32x4 acc, const u32x4& kop, int J) {
-          if constexpr (BF16) {
-            return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kop),
-                                                           __builtin_bit_cast(bf16x8, qr[J]), acc, 0, 0, 0);
+          if constexpr (W16) {
+            return mfma32<ELT>(kop, qr[J], acc);
           } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -937,8 +972,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         // of both blocks.  bf16: one transposed LDS read per block and d
         // block, in which lane t of the 16-lane group lg points at row
         // key + 4 lg + t / 4, columns 16 db + 4 (t % 4) .. + 3.
-        i16x4 vt[BF16 ? 2 * C::kDB : 1];
-        if constexpr (BF16) {
+        i16x4 vt[W16 ? 2 * C::kDB : 1];
+        if constexpr (W16) {
           typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
           const char* vrow = vs + (kb0 * kBlk + 4 * lg + (lm >> 2)) * C::kPitchV + 8 * (lm & 3);
 #pragma unroll
@@ -1003,18 +1038,16 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         }
 
         // O^T += V^T P^T
-        if constexpr (BF16) {
+        if constexpr (W16) {
           // 32-key contraction: element e of a lane's operands is key
           // 4 lg + e of block kb0 (e < 4) or key 4 lg + e - 4 of kb1
-          const u32x4 pb = {pack_bf16x2(pr[0], pr[1]), pack_bf16x2(pr[2], pr[3]), pack_bf16x2(pr[4], pr[5]),
-                            pack_bf16x2(pr[6], pr[7])};
+          const u32x4 pb = pack_p<ELT>(pr);
 #pragma unroll
           for (int db = 0; db < C::kDB; ++db) {
             const i16x4 a0 = vt[db], a1 = vt[C::kDB + db];
             const u32x4 va = {__builtin_bit_cast(uint2, a0).x, __builtin_bit_cast(uint2, a0).y,
                               __builtin_bit_cast(uint2, a1).x, __builtin_bit_cast(uint2, a1).y};
-            o[db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, va),
-                                                            __builtin_bit_cast(bf16x8, pb), o[db], 0, 0, 0);
+            o[db] = mfma32<ELT>(va, pb, o[db]);
           }
         } else {
           // f32: lane (lm, lg) takes V rows key + 4 lg + r at d = 16 db + lm
@@ -1164,8 +1197,12 @@ __global__ void zero_counters_kernel(int* counters, int n) {
 
 // ---------------------------------------------------------------- host side
 
+int elt_bytes(int dtype) { return dtype == SPECMOE_F32 ? 4 : 2; }
+
+bool known_dtype(int dtype) { return dtype == SPECMOE_F32 || dtype == SPECMOE_BF16 || dtype == SPECMOE_F16; }
+
 int key_tile(int dtype, int D) {
-  const int elt = dtype == SPECMOE_BF16 ? 2 : 4;
+  const int elt = elt_bytes(dtype);
   return kHalf / (D * elt);
 }
 
@@ -1180,7 +1217,7 @@ struct Plan {
 
 int validate_desc(const specmoe_verify_desc* d) {
   if (!d) return SPECMOE_ERR_NULL_POINTER;
-  if (d->dtype != SPECMOE_F32 && d->dtype != SPECMOE_BF16) return SPECMOE_ERR_DTYPE;
+  if (!known_dtype(d->dtype)) return SPECMOE_ERR_DTYPE;
   if (d->D != 64 && d->D != 128) return SPECMOE_ERR_HEAD_DIM;
   if (d->B < 0 || d->Hq <= 0 || d->Hkv <= 0 || d->C_max < 1 || d->S_max < d->C_max)
     return SPECMOE_ERR_SHAPE;
@@ -1196,7 +1233,7 @@ int validate_desc(const specmoe_verify_desc* d) {
   // byte offsets inside one (sequence, KV head) slab are 32-bit, packed
   // sequence lengths need T < 2^24, tile counts per launch stay in 32 bits.
   if ((int64_t)d->B * d->C_max * d->Hq >= ((int64_t)1 << 31)) return SPECMOE_ERR_SHAPE;
-  const int64_t elt = d->dtype == SPECMOE_BF16 ? 2 : 4;
+  const int64_t elt = elt_bytes(d->dtype);
   if ((int64_t)d->S_max * d->D * elt >= ((int64_t)1 << 31)) return SPECMOE_ERR_SHAPE;
   if (d->S_max >= (1 << 24)) return SPECMOE_ERR_SHAPE;
   const int64_t tile = key_tile(d->dtype, d->D);
@@ -1222,9 +1259,9 @@ Plan make_plan(const specmoe_verify_desc* d) {
   return pl;
 }
 
-template <bool BF16, int D, bool TREE>
+template <int ELT, int D, bool TREE>
 void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_desc* d) {
-  using C = Cfg<BF16, D>;
+  using C = Cfg<ELT != kF32, D>;
   const int B = p.B;
   if (d->ev_main_begin) (void)hipEventRecord(static_cast<hipEvent_t>(d->ev_main_begin), stream);
   // batches beyond kMaxSeqs sequences run as consecutive launches on the stream
@@ -1240,12 +1277,30 @@ void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_d
     if (TREE) s.draft_mask = p.draft_mask + (size_t)b0 * p.C_max;
     s.out = p.out + (size_t)b0 * p.C_max * p.Hq * D;
     s.lse = p.lse + (size_t)b0 * p.C_max * p.Hq;
-    hipLaunchKernelGGL((verify_attn_kernel<BF16, D, TREE>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE>), dim3(pl.P), dim3(kThreads), 0, stream, s);
   }
   if (d->ev_main_end) (void)hipEventRecord(static_cast<hipEvent_t>(d->ev_main_end), stream);
 }
 
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+template <int ELT>
+void launch_for_elt(int D, bool tree, const Params& p, const Plan& pl, hipStream_t s, const specmoe_verify_desc* d) {
+  if (tree) {
+    if (D == 128) launch<ELT, 128, true>(p, pl, s, d);
+    else launch<ELT, 64, true>(p, pl, s, d);
+  } else {
+    if (D == 128) launch<ELT, 128, false>(p, pl, s, d);
+    else launch<ELT, 64, false>(p, pl, s, d);
+  }
+}
+
+void launch_for(int dtype, int D, bool tree, const Params& p, const Plan& pl, hipStream_t s,
+                const specmoe_verify_desc* d) {
+  if (dtype == SPECMOE_BF16) launch_for_elt<kBF16>(D, tree, p, pl, s, d);
+  else if (dtype == SPECMOE_F16) launch_for_elt<kF16>(D, tree, p, pl, s, d);
+  else launch_for_elt<kF32>(D, tree, p, pl, s, d);
+}
 
 // Host checks and launch of both entry points; draft_mask is NULL for a
 // chain draft.
@@ -1293,18 +1348,7 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();  // clear a stale error from unrelated work
-  const bool bf16 = desc->dtype == SPECMOE_BF16;
-  if (tree) {
-    if (bf16 && desc->D == 128) launch<true, 128, true>(p, pl, s, desc);
-    else if (bf16) launch<true, 64, true>(p, pl, s, desc);
-    else if (desc->D == 128) launch<false, 128, true>(p, pl, s, desc);
-    else launch<false, 64, true>(p, pl, s, desc);
-  } else {
-    if (bf16 && desc->D == 128) launch<true, 128, false>(p, pl, s, desc);
-    else if (bf16) launch<true, 64, false>(p, pl, s, desc);
-    else if (desc->D == 128) launch<false, 128, false>(p, pl, s, desc);
-    else launch<false, 64, false>(p, pl, s, desc);
-  }
+  launch_for(desc->dtype, desc->D, tree, p, pl, s, desc);
   if (hipGetLastError() != hipSuccess) return SPECMOE_ERR_LAUNCH;
   return SPECMOE_OK;
 }
@@ -1335,7 +1379,7 @@ int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, 
 
 int32_t specmoe_verify_attn_key_tile(const specmoe_verify_desc* desc) {
   if (!desc) return SPECMOE_ERR_NULL_POINTER;
-  if (desc->dtype != SPECMOE_F32 && desc->dtype != SPECMOE_BF16) return SPECMOE_ERR_DTYPE;
+  if (!known_dtype(desc->dtype)) return SPECMOE_ERR_DTYPE;
   if (desc->D != 64 && desc->D != 128) return SPECMOE_ERR_HEAD_DIM;
   return key_tile(desc->dtype, desc->D);
 }

@@ -160,6 +160,8 @@ def test_key_tile(lib):
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=64))) == 128
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F32, D=128))) == 64
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(D=80))) == -4
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=bd.SPECMOE_F16))) == 128   # f16 as bf16
+    assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=3))) == -5
 
 
 def test_empty_batch_is_a_no_op(lib):

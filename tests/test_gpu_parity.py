@@ -19,7 +19,8 @@ from oracle import verify_attn_ref
 
 pytestmark = pytest.mark.gpu
 
-TOL = {"f32": (1e-4, 1e-4), "bf16": (1e-2, 1e-3)}
+TOL = {"f32": (1e-4, 1e-4), "bf16": (1e-2, 1e-3), "f16": (1e-2, 1e-3)}
+TORCH16 = {"bf16": torch.bfloat16, "f16": torch.float16}
 
 
 def dev():
@@ -29,8 +30,8 @@ def dev():
 
 
 def to_dev(a, dtype):
-    if dtype == "bf16":
-        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev())
+    if dtype in TORCH16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(TORCH16[dtype]).to(dev())
     return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev())
 
 
@@ -94,7 +95,7 @@ def test_tiny_fp32_full():
 
 
 @pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128",
-                                  "eagle_draft_b64"])
+                                  "eagle_draft_b64", "mixtral_f16_b64"])
 def test_workload_reduced_batch(name):
     """Every row of a few sequences drawn from each workload's distribution."""
     w = wl.get(name)
@@ -106,25 +107,26 @@ def test_workload_reduced_batch(name):
 
 
 def _full_size_inputs(w, sample):
-    """Full-size workload on the GPU: every sequence holds N(0,1) bf16 from
-    torch's generator except the sampled ones, which hold the recipe's values
-    (NaN-poisoned outside their valid rows) and are checked by the oracle."""
+    """Full-size workload on the GPU: every sequence holds N(0,1) values of the
+    workload's 16-bit type from torch's generator except the sampled ones,
+    which hold the recipe's values (NaN-poisoned outside their valid rows) and
+    are checked by the oracle."""
     ctx, chunk = wl.draw_lengths(w)
     d = dev()
     g = torch.Generator(device=d)
     g.manual_seed(1000 + w.index)
     shape = (w.B, w.Hkv, w.S_max, w.D)
-    k = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(torch.bfloat16)
-    v = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(torch.bfloat16)
+    k = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(TORCH16[w.dtype])
+    v = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(TORCH16[w.dtype])
     host = wl.make_inputs(w, batches=sample)
     for b in sample:
-        k[b] = to_dev(host["k_cache"][b], "bf16")
-        v[b] = to_dev(host["v_cache"][b], "bf16")
-    return host, to_dev(host["q"], "bf16"), k, v, ctx, chunk
+        k[b] = to_dev(host["k_cache"][b], w.dtype)
+        v[b] = to_dev(host["v_cache"][b], w.dtype)
+    return host, to_dev(host["q"], w.dtype), k, v, ctx, chunk
 
 
 @pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128",
-                                  "eagle_draft_b64"])
+                                  "eagle_draft_b64", "mixtral_f16_b64"])
 def test_workload_full_size_sampled(name):
     """Full-size workload in the benchmark's launch configuration (default
     grid); the oracle checks sampled sequences, every output row is
@@ -178,6 +180,10 @@ EDGE = {
     "f32_d64_three_blocks": (2, 16, 2, 64, "f32", [200, 150], [5, 6], 6),
     "mha_g1": (3, 8, 8, 128, "bf16", [400, 10, 1000], [4, 2, 3], 4),
     "bf16_d64": (3, 16, 4, 64, "bf16", [500, 260, 1], [5, 3, 5], 5),
+    # f16 (the paper's KV precision): both head dims, ragged, three row blocks
+    "f16_d64": (3, 16, 4, 64, "f16", [500, 260, 1], [5, 3, 5], 5),
+    "f16_three_row_tiles": (4, 28, 4, 128, "f16", [700, 33, 1500, 2], [10, 12, 13, 16], 16),
+    "f16_tile_boundaries": (6, 8, 2, 128, "f16", [123, 127, 128, 129, 255, 507], [5, 1, 2, 5, 1, 5], 5),
     "f32_d128": (2, 8, 2, 128, "f32", [300, 77], [4, 2], 4),
     "f32_d64_many": (3, 12, 3, 64, "f32", [1000, 5, 640], [3, 8, 1], 8),
     # chunks longer than a key tile (f32, D=128: 64-key tiles): some tiles

@@ -107,6 +107,7 @@ TREE_EDGE = {
     # third word is empty, so such a piece holds rows that see no key in it
     "f32_d128_draft_fills_tile": (3, 2, 1, 128, "f32", [64, 0, 128], [64, 64, 64], 64, "holes"),
     "bf16_d64_random": (3, 16, 4, 64, "bf16", [500, 0, 1], [5, 3, 5], 5, "random"),
+    "f16_random_trees_g7": (5, 28, 4, 128, "f16", [700, 33, 1500, 2, 260], [10, 1, 16, 13, 7], 16, "tree"),
     "f32_d64_random_junk": (3, 12, 3, 64, "f32", [1000, 0, 640], [3, 8, 1], 8, "random_junk"),
     # no context and sparse masks: rows that see no key at all
     "empty_rows_no_context": (4, 8, 2, 128, "bf16", [0, 0, 0, 5], [6, 2, 9, 4], 9, "sparse"),
