@@ -134,6 +134,27 @@ def chunked_attention(Q: np.ndarray, K: np.ndarray, V: np.ndarray, M: np.ndarray
     return out, lse
 
 
+def gather_pages(pages: np.ndarray, block_table, page_size: int) -> np.ndarray:
+    """A paged KV cache written out as the contiguous [B, Hkv, S_max, D] one.
+
+    ``pages`` is [num_pages, Hkv, page_size, D]; ``block_table`` [B, P] lists
+    each sequence's pages in order: token j of sequence b sits in page
+    block_table[b, j // page_size] at row j % page_size, so S_max = P *
+    page_size.  (Paged storage is not the paper's: Section 2.2 only cites KV
+    cache managers; this layout is the build's own.)
+    """
+    table = np.asarray(block_table)
+    B, P = table.shape
+    _, Hkv, ps, D = pages.shape
+    if ps != page_size:
+        raise ValueError("pages and page_size disagree")
+    out = np.empty((B, Hkv, P * ps, D), dtype=pages.dtype)
+    for b in range(B):
+        for t in range(P):
+            out[b, :, t * ps:(t + 1) * ps] = pages[int(table[b, t])]
+    return out
+
+
 def verify_attn_ref(q, k_cache, v_cache, ctx_lens, chunk_lens, scale: float,
                     dtype: str, units=None, draft_mask=None):
     """Chunked verification attention for a batch of sequences, in float64.

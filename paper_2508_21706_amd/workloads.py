@@ -35,6 +35,12 @@ Recipe (all draws with numpy's PCG64 ``default_rng``):
     bf16 (binary16); the same bits feed the GPU and the oracle.
   * Rows that hold no valid data (cache rows >= T_b, query rows >= c_b) are
     filled with ``fill`` (NaN by default) so that any read of them shows up.
+  * Paged caches (workloads with ``page_size`` > 0): the contiguous cache is
+    cut into pages of ``page_size`` tokens, [num_pages, Hkv, page_size, D],
+    placed in a pool of B * S_max / page_size + 8 pages at the positions of
+    ``default_rng([seed, 5]).permutation``; the block table [B, S_max /
+    page_size] lists each sequence's pages in order; unused pages hold
+    ``fill``.
   * Tree drafts (workloads with ``draft="tree"``): the draft tokens of
     sequence b form a random recursive tree drawn with
     ``default_rng([seed, 3, b])``: token 0 is the root and token i >= 1 hangs
@@ -68,6 +74,7 @@ class Workload:
     chunk: tuple          # ("fixed", n) | ("uniform", lo, hi)
     description: str
     draft: str = "chain"  # "chain", or "tree": a random tree with draft-mask words
+    page_size: int = 0    # 0: contiguous KV cache; else tokens per page of a paged cache
 
     @property
     def group(self) -> int:
@@ -127,6 +134,10 @@ WORKLOADS = [
              ctx=("uniform", 512, 2048), chunk=("fixed", 5),
              description="Mixtral-8x7B attention shape with an FP16 KV cache (the paper's precision): B=64, "
                          "Hq=32, Hkv=8, D=128, ctx U[512,2048], chunk 5"),
+    Workload("mixtral_paged_b64", 9, B=64, Hq=32, Hkv=8, D=128, dtype="bf16",
+             ctx=("uniform", 512, 2048), chunk=("fixed", 5), page_size=16,
+             description="Mixtral-8x7B attention shape with a paged KV cache (16-token pages in a shuffled "
+                         "pool), bf16: B=64, Hq=32, Hkv=8, D=128, ctx U[512,2048], chunk 5"),
     Workload("eagle_draft_b64", 7, B=64, Hq=32, Hkv=32, D=128, dtype="bf16",
              ctx=("uniform", 512, 2048), chunk=("fixed", 1),
              description="draft-model decode attention (one MHA layer of the EAGLE draft for Mixtral-8x7B), "
@@ -243,8 +254,32 @@ def make_inputs(w: Workload, fill: float = float("nan"),
         k[b, :, :T_b] = kv_slab(w, b, T_b, "k")
         v[b, :, :T_b] = kv_slab(w, b, T_b, "v")
     draft_mask = tree_draft_masks(w.index, chunk, w.C_max) if w.draft == "tree" else None
-    return dict(q=q, k_cache=k, v_cache=v, ctx_lens=ctx, chunk_lens=chunk,
-                scale=w.scale, workload=w, draft_mask=draft_mask)
+    out = dict(q=q, k_cache=k, v_cache=v, ctx_lens=ctx, chunk_lens=chunk,
+               scale=w.scale, workload=w, draft_mask=draft_mask)
+    if w.page_size:
+        out["k_pages"], out["block_table"] = paginate(k, w.page_size, w.index, fv)
+        out["v_pages"], _ = paginate(v, w.page_size, w.index, fv)
+    return out
+
+
+def paginate(cache: np.ndarray, page_size: int, seed: int, fill, spare: int = 8):
+    """Cut a contiguous [B, Hkv, S_max, D] cache into a shuffled pool of pages
+    [B * S_max / page_size + spare, Hkv, page_size, D] and its block table
+    [B, S_max / page_size] (int32): token j of sequence b lands in page
+    table[b, j // page_size], row j % page_size.  The pool positions come
+    from ``default_rng([seed, 5]).permutation``, the same for K and V; spare
+    pages hold ``fill``.  Input preparation only."""
+    B, Hkv, S, D = cache.shape
+    if S % page_size:
+        raise ValueError("S_max must be a multiple of page_size")
+    P = S // page_size
+    perm = np.random.default_rng([seed, 5]).permutation(B * P + spare)
+    table = perm[: B * P].reshape(B, P).astype(np.int32)
+    pages = np.full((B * P + spare, Hkv, page_size, D), fill, dtype=cache.dtype)
+    for b in range(B):
+        for t in range(P):
+            pages[table[b, t]] = cache[b, :, t * page_size:(t + 1) * page_size]
+    return pages, table
 
 
 def tree_draft_masks(seed: int, chunk_lens, C_max: int) -> np.ndarray:

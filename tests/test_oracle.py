@@ -547,3 +547,56 @@ def test_tree_masks_are_root_paths():
     inp = wl.make_inputs(wl.dataclasses.replace(w6, B=2), batches=[])
     assert inp["draft_mask"].shape == (2, 16) and inp["draft_mask"][0, 0] == 1
     assert wl.make_inputs(wl.dataclasses.replace(wl.get(1)))["draft_mask"] is None
+
+
+# ------------------------------------------------------------ paged caches
+
+def test_gather_pages_identity_and_shuffled():
+    """Pages cut from a contiguous cache in order gather back to it exactly;
+    a shuffled pool with its table gives the same attention results."""
+    rng = np.random.default_rng(51)
+    q, k, v, ctx, chunk = _rand_case(rng, B=3, ctx=(20, 3, 41), chunk=(4, 2, 3), C_max=4, S_pad=0)
+    S = int((ctx + chunk).max())
+    S = (S + 7) // 8 * 8
+    k = np.pad(k, ((0, 0), (0, 0), (0, S - k.shape[2]), (0, 0)))
+    v = np.pad(v, ((0, 0), (0, 0), (0, S - v.shape[2]), (0, 0)))
+    ps, P = 8, S // 8
+    ident = np.arange(3 * P, dtype=np.int32).reshape(3, P)
+    pages = k.reshape(3, k.shape[1], P, ps, k.shape[3]).transpose(0, 2, 1, 3, 4).reshape(3 * P, k.shape[1], ps, -1)
+    assert np.array_equal(oracle_mod.gather_pages(pages, ident, ps), k)
+    kp, table = wl.paginate(k, ps, 7, np.float32(np.nan))
+    vp, table_v = wl.paginate(v, ps, 7, np.float32(np.nan))
+    assert np.array_equal(table, table_v) and len(np.unique(table)) == table.size
+    assert np.all(np.isnan(np.delete(kp, table.ravel(), axis=0)))     # spare pages are poisoned
+    o1, s1 = oracle_mod.verify_attn_ref(q, k, v, ctx, chunk, 0.3, "f32")
+    o2, s2 = oracle_mod.verify_attn_ref(q, oracle_mod.gather_pages(kp, table, ps),
+                                        oracle_mod.gather_pages(vp, table, ps), ctx, chunk, 0.3, "f32")
+    np.testing.assert_array_equal(o1, o2)
+    np.testing.assert_array_equal(s1, s2)
+
+
+@pytest.mark.parametrize("old,new", [
+    ("pages[int(table[b, t])]", "pages[int(table[b, P - 1 - t])]"),          # pages out of order
+    ("pages[int(table[b, t])]", "pages[int(table[b, t])][:, ::-1]"),         # rows reversed in a page
+    ("pages[int(table[b, t])]", "pages[int(table[(b + 1) % B, t])]"),        # another sequence's table
+])
+def test_gather_pages_catches_planted_mistake(old, new):
+    with open(oracle_mod.__file__) as f:
+        src = f.read()
+    _gather_pin(oracle_mod)
+    mod = _mutant(src, old, new)
+    with pytest.raises(AssertionError):
+        _gather_pin(mod)
+
+
+def _gather_pin(m):
+    """Pages in order gather back to the cache they were cut from; so does a
+    shuffled pool through its table."""
+    rng = np.random.default_rng(52)
+    k = rng.standard_normal((3, 2, 24, 4)).astype(np.float32)
+    ps, P = 8, 3
+    ident = np.arange(3 * P, dtype=np.int32).reshape(3, P)
+    pages = k.reshape(3, 2, P, ps, 4).transpose(0, 2, 1, 3, 4).reshape(3 * P, 2, ps, 4)
+    assert np.array_equal(m.gather_pages(pages, ident, ps), k)
+    kp, table = wl.paginate(k, ps, 3, np.float32(np.nan))
+    assert np.array_equal(m.gather_pages(kp, table, ps), k)
