@@ -260,15 +260,18 @@ def main():
             return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(t16).to(dev)
         return torch.from_numpy(a).to(dev)
 
-    set_bytes = inp["k_cache"].nbytes * 2
+    paged = w.page_size > 0
+    kname, vname = ("k_pages", "v_pages") if paged else ("k_cache", "v_cache")
+    set_bytes = inp[kname].nbytes * 2
     n_sets = args.rotate or max(4, int(np.ceil(1.0e9 / set_bytes)))
     q = to_dev(inp["q"])
-    k0, v0 = to_dev(inp["k_cache"]), to_dev(inp["v_cache"])
+    k0, v0 = to_dev(inp[kname]), to_dev(inp[vname])
+    table_d = torch.from_numpy(inp["block_table"]).to(dev) if paged else None
     sets = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(n_sets - 1)]
     ctx_d = torch.from_numpy(ctx).to(dev)
     chunk_d = torch.from_numpy(chunk).to(dev)
     mask_d = torch.from_numpy(inp["draft_mask"].view(np.int64)).to(dev) if tree else None
-    desc = pkg.desc_for(q, k0, args.grid_blocks)
+    desc = pkg.make_desc(w.B, w.Hq, w.Hkv, w.D, w.C_max, w.S_max, pkg.binding._dtype_code(q), args.grid_blocks)
     ws = pkg.alloc_workspace(desc, dev)
     out = torch.empty((w.B, w.C_max, w.Hq, w.D), dtype=torch.float32, device=dev)
     lse = torch.empty((w.B, w.C_max, w.Hq), dtype=torch.float32, device=dev)
@@ -278,7 +281,10 @@ def main():
 
     def step(i, events=None):
         k, v = sets[i % n_sets]
-        if tree:
+        if paged:
+            pkg.verify_attn_paged(q, k, v, table_d, ctx_d, chunk_d, w.scale, draft_mask=mask_d, out=out, lse=lse,
+                                  workspace=ws, grid_blocks=args.grid_blocks, stream=stream, events=events)
+        elif tree:
             pkg.verify_attn_tree(q, k, v, ctx_d, chunk_d, mask_d, w.scale, out=out, lse=lse, workspace=ws,
                                  grid_blocks=args.grid_blocks, stream=stream, events=events)
         else:
@@ -339,7 +345,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
                    "head_dim": w.D, "ctx_lens_sum": int(ctx.sum()), "chunk_lens_sum": tokens,
-                   "C_max": w.C_max, "S_max": w.S_max, "draft": w.draft,
+                   "C_max": w.C_max, "S_max": w.S_max, "draft": w.draft, "page_size": w.page_size,
                    "grid_blocks": args.grid_blocks or 256,
                    "input_sets": n_sets,
                    "parallelism": "single GPU"},

@@ -55,8 +55,11 @@ enum {
   SPECMOE_ERR_SCALE = -10,        /* scale is not finite                              */
   SPECMOE_ERR_LAUNCH = -11,       /* HIP reported an error for a kernel launch        */
   SPECMOE_ERR_FLAGS = -12,        /* flags is not 0                                   */
-  SPECMOE_ERR_MASK = -13          /* a draft mask with C_max > 64 (one 64-bit word per
+  SPECMOE_ERR_MASK = -13,         /* a draft mask with C_max > 64 (one 64-bit word per
                                      draft token covers at most 64 draft tokens)      */
+  SPECMOE_ERR_PAGES = -14         /* paged cache: page_size not a power of two in
+                                     [8, 65536], pages_per_seq or num_pages < 1, or
+                                     S_max != page_size * pages_per_seq               */
 };
 
 /* Problem description.  Sizes are in elements unless stated otherwise. */
@@ -165,6 +168,46 @@ int specmoe_verify_attn_tree(const void* q, const void* k_cache, const void* v_c
                              const int32_t* ctx_lens, const int32_t* chunk_lens,
                              const uint64_t* draft_mask, float scale, float* out, float* lse,
                              void* stream, const specmoe_verify_desc* desc);
+
+/* Geometry of a paged KV cache (host struct). */
+typedef struct specmoe_paged_kv {
+  int32_t page_size;      /* tokens per page: a power of two in [8, 65536]            */
+  int32_t pages_per_seq;  /* columns of the block table; desc->S_max must equal
+                             page_size * pages_per_seq                               */
+  int32_t num_pages;      /* pages in the pool                                        */
+} specmoe_paged_kv;
+
+/*
+ * specmoe_verify_attn_paged -- chunked verification attention over a paged
+ * KV cache.
+ *
+ * The operation of specmoe_verify_attn (or, with a draft_mask, of
+ * specmoe_verify_attn_tree), with the KV cache held as a pool of pages
+ * instead of one slab per sequence.  Paging is not part of the paper
+ * (Section 2.2 only cites KV-cache managers); this layout is the library's:
+ *
+ *   k_pages, v_pages  [num_pages, Hkv, page_size, D] dtype, device, 16-byte
+ *                aligned: page P holds page_size consecutive tokens of one
+ *                sequence for every KV head.
+ *   block_table  int32 [B, pages_per_seq], device: token j of sequence b is
+ *                in page block_table[b * pages_per_seq + j / page_size], row
+ *                j % page_size.  Only the entries that cover tokens
+ *                [0, l_b + c_b) are read; an entry outside [0, num_pages) is
+ *                clamped into it (unspecified values, never an out-of-bounds
+ *                access).
+ *   draft_mask   NULL for chain drafts, else as in specmoe_verify_attn_tree.
+ *   paged        host pointer to the page geometry.
+ *
+ * Every other argument, the workspace, the preconditions (with
+ * S_max = page_size * pages_per_seq), ownership, determinism and the errors
+ * are those of specmoe_verify_attn; SPECMOE_ERR_PAGES reports a bad geometry,
+ * SPECMOE_ERR_NULL_POINTER a NULL paged or (with B > 0) block_table.
+ */
+int specmoe_verify_attn_paged(const void* q, const void* k_pages, const void* v_pages,
+                              const int32_t* block_table, const int32_t* ctx_lens,
+                              const int32_t* chunk_lens, const uint64_t* draft_mask, float scale,
+                              float* out, float* lse, void* stream, const specmoe_verify_desc* desc,
+                              const specmoe_paged_kv* paged);
 
 /* Bytes of device workspace specmoe_verify_attn needs for `desc` (its
  * grid_blocks included); 0 for an invalid descriptor.  The workspace starts

@@ -24,7 +24,7 @@ STATUS = {
     0: "SPECMOE_OK", -1: "SPECMOE_ERR_NULL_POINTER", -2: "SPECMOE_ERR_SHAPE", -3: "SPECMOE_ERR_GQA",
     -4: "SPECMOE_ERR_HEAD_DIM", -5: "SPECMOE_ERR_DTYPE", -6: "SPECMOE_ERR_ROWS", -7: "SPECMOE_ERR_GRID",
     -8: "SPECMOE_ERR_WORKSPACE", -9: "SPECMOE_ERR_ALIGN", -10: "SPECMOE_ERR_SCALE", -11: "SPECMOE_ERR_LAUNCH",
-    -12: "SPECMOE_ERR_FLAGS", -13: "SPECMOE_ERR_MASK",
+    -12: "SPECMOE_ERR_FLAGS", -13: "SPECMOE_ERR_MASK", -14: "SPECMOE_ERR_PAGES",
 }
 
 
@@ -46,6 +46,11 @@ class AcceptDesc(ctypes.Structure):
         ("split", ctypes.c_int32), ("flags", ctypes.c_int32),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
     ]
+
+
+class PagedKV(ctypes.Structure):
+    """Mirror of ``specmoe_paged_kv``."""
+    _fields_ = [("page_size", ctypes.c_int32), ("pages_per_seq", ctypes.c_int32), ("num_pages", ctypes.c_int32)]
 
 
 class SpecMoEError(RuntimeError):
@@ -75,6 +80,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.specmoe_verify_attn_tree.argtypes = [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_paged.restype = ctypes.c_int
+    lib.specmoe_verify_attn_paged.argtypes = [ctypes.c_void_p] * 7 + [
+        ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Desc), ctypes.POINTER(PagedKV)]
     lib.specmoe_verify_attn_workspace_bytes.restype = ctypes.c_size_t
     lib.specmoe_verify_attn_workspace_bytes.argtypes = [ctypes.POINTER(Desc)]
     lib.specmoe_verify_attn_workspace_init.restype = ctypes.c_int
@@ -198,17 +206,49 @@ def verify_attn_tree(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
                  grid_blocks, stream, events, check_lengths)
 
 
+def verify_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor, block_table: torch.Tensor,
+                      ctx_lens: torch.Tensor, chunk_lens: torch.Tensor, scale: float,
+                      draft_mask: Optional[torch.Tensor] = None,
+                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                      workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
+                      stream: Optional[torch.cuda.Stream] = None, events=None,
+                      check_lengths: bool = False):
+    """Chunked verification attention over a paged KV cache; see
+    ``specmoe_verify_attn_paged`` in ``include/specmoe_verify.h``.
+
+    k_pages / v_pages [num_pages, Hkv, page_size, D], block_table int32
+    [B, pages_per_seq] (S_max = page_size * pages_per_seq); the other
+    arguments as ``verify_attn`` (``draft_mask``: tree drafts, as
+    ``verify_attn_tree``).
+    """
+    if k_pages.dim() != 4:
+        raise ValueError("k_pages must be [num_pages, Hkv, page_size, D]")
+    num_pages, _, page_size, _ = k_pages.shape
+    if block_table.dim() != 2:
+        raise ValueError("block_table must be [B, pages_per_seq]")
+    _check(block_table, "block_table", (q.shape[0], block_table.shape[1]), torch.int32)
+    paged = PagedKV(page_size, block_table.shape[1], num_pages)
+    return _call(q, k_pages, v_pages, ctx_lens, chunk_lens, draft_mask, scale, out, lse, workspace, grid_blocks,
+                 stream, events, check_lengths, paged=paged, block_table=block_table)
+
+
 def _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse, workspace, grid_blocks,
-          stream, events, check_lengths):
+          stream, events, check_lengths, paged: Optional[PagedKV] = None, block_table=None):
     lib = load_library()
     B, C_max, Hq, D = q.shape
     if k_cache.dim() != 4:
         raise ValueError("k_cache must be [B, Hkv, S_max, D]")
-    _, Hkv, S_max, _ = k_cache.shape
     dt = q.dtype
     _check(q, "q", (B, C_max, Hq, D), dt)
-    _check(k_cache, "k_cache", (B, Hkv, S_max, D), dt)
-    _check(v_cache, "v_cache", (B, Hkv, S_max, D), dt)
+    if paged is None:
+        _, Hkv, S_max, _ = k_cache.shape
+        _check(k_cache, "k_cache", (B, Hkv, S_max, D), dt)
+        _check(v_cache, "v_cache", (B, Hkv, S_max, D), dt)
+    else:
+        Hkv = k_cache.shape[1]
+        S_max = paged.page_size * paged.pages_per_seq
+        _check(k_cache, "k_pages", (paged.num_pages, Hkv, paged.page_size, D), dt)
+        _check(v_cache, "v_pages", (paged.num_pages, Hkv, paged.page_size, D), dt)
     _check(ctx_lens, "ctx_lens", (B,), torch.int32)
     _check(chunk_lens, "chunk_lens", (B,), torch.int32)
     if draft_mask is not None:
@@ -235,7 +275,13 @@ def _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse
     desc.workspace_bytes = workspace.numel() * workspace.element_size()
     if events is not None:
         desc.ev_main_begin, desc.ev_main_end = events
-    if draft_mask is None:
+    if paged is not None:
+        st = lib.specmoe_verify_attn_paged(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
+                                           block_table.data_ptr(), ctx_lens.data_ptr(), chunk_lens.data_ptr(),
+                                           draft_mask.data_ptr() if draft_mask is not None else None,
+                                           float(scale), out.data_ptr(), lse.data_ptr(), s.cuda_stream,
+                                           ctypes.byref(desc), ctypes.byref(paged))
+    elif draft_mask is None:
         st = lib.specmoe_verify_attn(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                      ctx_lens.data_ptr(), chunk_lens.data_ptr(), float(scale),
                                      out.data_ptr(), lse.data_ptr(), s.cuda_stream, ctypes.byref(desc))

@@ -121,6 +121,9 @@ struct Params {
   int P;            // persistent workgroups
   float sl2;        // scale * log2(e)
   const uint64_t* draft_mask;   // [B][C_max] draft-mask words (tree drafts only)
+  // paged caches only: k and v are [num_pages][Hkv][1 << page_shift][D]
+  const int32_t* block_table;   // [B][pages_per_seq]
+  int page_shift, pages_per_seq, num_pages;
 };
 
 // W16: 16-bit elements (bf16 or f16), which share every layout
@@ -433,8 +436,9 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
 }
 
 // TREE: the draft region obeys per-token draft-mask words instead of the
-// chain mask.
-template <int ELT, int D, bool TREE>
+// chain mask.  PAGED: the KV cache is a pool of pages found through a block
+// table.
+template <int ELT, int D, bool TREE, bool PAGED>
 __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   constexpr bool W16 = ELT != kF32;   // 16-bit elements
   using C = Cfg<W16, D>;
@@ -642,7 +646,23 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // masked key (probability 0) always meets finite V values.  The two waves of a producer pair issue the K and V
   // instructions of even and odd index.
   const int pw = wave & 1;
-  auto dma = [&](const Cursor& cu, int st) {
+  // (paged) the pool pages of the tile of cu, one per lane of a producer
+  // wave: lane l holds the page of the tile's l-th page (at most 33 of them:
+  // pages hold at least 8 tokens, tiles at most 256).  Out-of-range table
+  // entries are clamped into the pool.
+  auto load_pages = [&](const Cursor& cu) {
+    int r = 0;
+    if constexpr (PAGED) {
+      const int T = seq_T(cu.s);
+      const int hi = T - (seq_tiles<C>(cu.s) - 1 - cu.j) * C::kTileKeys;
+      const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
+      const int fp = lo >> p.page_shift;
+      if (lane <= ((hi - 1) >> p.page_shift) - fp)
+        r = min(max(p.block_table[(size_t)cu.b * p.pages_per_seq + fp + lane], 0), p.num_pages - 1);
+    }
+    return r;
+  };
+  auto dma = [&](const Cursor& cu, int st, int pg) {
     const int T = seq_T(cu.s);
     const int hi = T - (seq_tiles<C>(cu.s) - 1 - cu.j) * C::kTileKeys;
     const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
@@ -665,13 +685,29 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       const int vrow_ = sl / C::kSlotsV;
       const uint32_t voff =
           (uint32_t)min(vrow_, last) * C::kRowBytes + 16u * min(sl - vrow_ * C::kSlotsV, C::kChunks - 1);
+      const char* ksrc = kp + koff;
+      const char* vsrc = vp + voff;
+      if constexpr (PAGED) {
+        // row j of the sequence: page table[j >> shift] of the pool, row
+        // j & (page - 1) of the unit's KV head in it
+        const int sh = p.page_shift;
+        const int fp = lo >> sh;
+        const size_t page_bytes = ((size_t)Hkv << sh) * C::kRowBytes;
+        const size_t head_bytes = ((size_t)cu.kvh << sh) * C::kRowBytes;
+        const int kj = lo + min(krow_, last), vj = lo + min(vrow_, last);
+        const int kpage = __shfl(pg, (kj >> sh) - fp), vpage = __shfl(pg, (vj >> sh) - fp);
+        ksrc = p.k + (size_t)kpage * page_bytes + head_bytes + (size_t)(kj & ((1 << sh) - 1)) * C::kRowBytes +
+               16u * min(sl - krow_ * C::kSlotsK, C::kChunks - 1);
+        vsrc = p.v + (size_t)vpage * page_bytes + head_bytes + (size_t)(vj & ((1 << sh) - 1)) * C::kRowBytes +
+               16u * min(sl - vrow_ * C::kSlotsV, C::kChunks - 1);
+      }
       // a K load whose first row is past the tile's keys is skipped: those
       // scores are masked whatever the slots hold
       if (i < C::kInstK && sl < C::kTileKeys * C::kSlotsK && (64 * i) / C::kSlotsK <= last)
-        __builtin_amdgcn_global_load_lds(kp + koff, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
+        __builtin_amdgcn_global_load_lds(ksrc, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
                                          kStreaming);
       if (i < C::kInstV && sl < C::kTileKeys * C::kSlotsV)
-        __builtin_amdgcn_global_load_lds(vp + voff, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0,
+        __builtin_amdgcn_global_load_lds(vsrc, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0,
                                          kStreaming);
     }
   };
@@ -785,15 +821,28 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     Cursor cu = first;
     int v = grp;
     if (grp == 1 && count > 1) advance(cu, 0);
+    int pg = 0;   // (paged) the pages of the pair's next tile
+    if constexpr (PAGED)
+      if (v < count) pg = load_pages(cu);
     for (; v < count; v += 2) {
       if (v >= 2) wait_count(&empty_cnt[grp], kConsumers * (v >> 1));
       if (v == 1) wait_count(&full_cnt[0], 2);
-      dma(cu, grp);
+      dma(cu, grp, pg);
+      if constexpr (PAGED) {
+        // the next tile's table entries ride the wait for this tile's loads
+        if (v + 2 < count) {
+          advance(cu, v);
+          advance(cu, v + 1);
+          pg = load_pages(cu);
+        }
+      }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       signal_count(&full_cnt[grp]);
-      if (v + 2 < count) {
-        advance(cu, v);
-        advance(cu, v + 1);
+      if constexpr (!PAGED) {
+        if (v + 2 < count) {
+          advance(cu, v);
+          advance(cu, v + 1);
+        }
       }
     }
     return;
@@ -1259,7 +1308,7 @@ Plan make_plan(const specmoe_verify_desc* d) {
   return pl;
 }
 
-template <int ELT, int D, bool TREE>
+template <int ELT, int D, bool TREE, bool PAGED>
 void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_desc* d) {
   using C = Cfg<ELT != kF32, D>;
   const int B = p.B;
@@ -1269,53 +1318,84 @@ void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_d
     Params s = p;
     s.B = B - b0 < kMaxSeqs ? B - b0 : kMaxSeqs;
     s.q = p.q + (size_t)b0 * p.C_max * p.Hq * C::kRowBytes;
-    const size_t slab = (size_t)b0 * p.Hkv * p.S_max * C::kRowBytes;
-    s.k = p.k + slab;
-    s.v = p.v + slab;
+    if (PAGED) {
+      s.block_table = p.block_table + (size_t)b0 * p.pages_per_seq;
+    } else {
+      const size_t slab = (size_t)b0 * p.Hkv * p.S_max * C::kRowBytes;
+      s.k = p.k + slab;
+      s.v = p.v + slab;
+    }
     s.ctx_lens = p.ctx_lens + b0;
     s.chunk_lens = p.chunk_lens + b0;
     if (TREE) s.draft_mask = p.draft_mask + (size_t)b0 * p.C_max;
     s.out = p.out + (size_t)b0 * p.C_max * p.Hq * D;
     s.lse = p.lse + (size_t)b0 * p.C_max * p.Hq;
-    hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED>), dim3(pl.P), dim3(kThreads), 0, stream, s);
   }
   if (d->ev_main_end) (void)hipEventRecord(static_cast<hipEvent_t>(d->ev_main_end), stream);
 }
 
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
-template <int ELT>
+template <int ELT, bool PAGED>
 void launch_for_elt(int D, bool tree, const Params& p, const Plan& pl, hipStream_t s, const specmoe_verify_desc* d) {
   if (tree) {
-    if (D == 128) launch<ELT, 128, true>(p, pl, s, d);
-    else launch<ELT, 64, true>(p, pl, s, d);
+    if (D == 128) launch<ELT, 128, true, PAGED>(p, pl, s, d);
+    else launch<ELT, 64, true, PAGED>(p, pl, s, d);
   } else {
-    if (D == 128) launch<ELT, 128, false>(p, pl, s, d);
-    else launch<ELT, 64, false>(p, pl, s, d);
+    if (D == 128) launch<ELT, 128, false, PAGED>(p, pl, s, d);
+    else launch<ELT, 64, false, PAGED>(p, pl, s, d);
   }
 }
 
-void launch_for(int dtype, int D, bool tree, const Params& p, const Plan& pl, hipStream_t s,
+template <bool PAGED>
+void launch_for_paging(int dtype, int D, bool tree, const Params& p, const Plan& pl, hipStream_t s,
+                       const specmoe_verify_desc* d) {
+  if (dtype == SPECMOE_BF16) launch_for_elt<kBF16, PAGED>(D, tree, p, pl, s, d);
+  else if (dtype == SPECMOE_F16) launch_for_elt<kF16, PAGED>(D, tree, p, pl, s, d);
+  else launch_for_elt<kF32, PAGED>(D, tree, p, pl, s, d);
+}
+
+void launch_for(int dtype, int D, bool tree, bool paged, const Params& p, const Plan& pl, hipStream_t s,
                 const specmoe_verify_desc* d) {
-  if (dtype == SPECMOE_BF16) launch_for_elt<kBF16>(D, tree, p, pl, s, d);
-  else if (dtype == SPECMOE_F16) launch_for_elt<kF16>(D, tree, p, pl, s, d);
-  else launch_for_elt<kF32>(D, tree, p, pl, s, d);
+  if (paged) launch_for_paging<true>(dtype, D, tree, p, pl, s, d);
+  else launch_for_paging<false>(dtype, D, tree, p, pl, s, d);
 }
 
 // Host checks and launch of both entry points; draft_mask is NULL for a
 // chain draft.
+// Page geometry of a paged call: page_size a power of two in [8, 65536]
+// (tiles hold at most 256 keys, so a tile meets at most 33 pages, one per
+// producer lane), S_max = page_size * pages_per_seq, a non-empty pool.
+int validate_pages(const specmoe_verify_desc* d, const specmoe_paged_kv* pk) {
+  if (!pk) return SPECMOE_ERR_NULL_POINTER;
+  const int ps = pk->page_size;
+  if (ps < 8 || ps > 65536 || (ps & (ps - 1)) != 0) return SPECMOE_ERR_PAGES;
+  if (pk->pages_per_seq < 1 || pk->num_pages < 1) return SPECMOE_ERR_PAGES;
+  if ((int64_t)ps * pk->pages_per_seq != d->S_max) return SPECMOE_ERR_PAGES;
+  if ((int64_t)kMaxSeqs * pk->pages_per_seq >= ((int64_t)1 << 31)) return SPECMOE_ERR_PAGES;
+  return SPECMOE_OK;
+}
+
 int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* ctx_lens,
         const int32_t* chunk_lens, const uint64_t* draft_mask, bool tree, float scale, float* out, float* lse,
-        void* stream, const specmoe_verify_desc* desc) {
+        void* stream, const specmoe_verify_desc* desc, const int32_t* block_table = nullptr,
+        const specmoe_paged_kv* paged = nullptr) {
   const int st = validate_desc(desc);
   if (st != SPECMOE_OK) return st;
   if (tree && desc->C_max > kMaxDraftBits) return SPECMOE_ERR_MASK;
+  const bool is_paged = paged != nullptr;
+  if (is_paged) {
+    const int sp = validate_pages(desc, paged);
+    if (sp != SPECMOE_OK) return sp;
+  }
   if (desc->B == 0) return SPECMOE_OK;   // nothing to read or write
   if (!q || !k_cache || !v_cache || !ctx_lens || !chunk_lens || !out || !lse) return SPECMOE_ERR_NULL_POINTER;
   if (tree && !draft_mask) return SPECMOE_ERR_NULL_POINTER;
   if (!isfinite(scale)) return SPECMOE_ERR_SCALE;
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return SPECMOE_ERR_ALIGN;
   if (tree && (reinterpret_cast<uintptr_t>(draft_mask) & 7u) != 0) return SPECMOE_ERR_ALIGN;
+  if (is_paged && !block_table) return SPECMOE_ERR_NULL_POINTER;
   const Plan pl = make_plan(desc);
   if (!desc->workspace) return SPECMOE_ERR_NULL_POINTER;
   if (!aligned16(desc->workspace)) return SPECMOE_ERR_ALIGN;
@@ -1330,6 +1410,10 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   p.out = out;
   p.lse = lse;
   p.draft_mask = draft_mask;
+  p.block_table = block_table;
+  p.page_shift = is_paged ? __builtin_ctz((unsigned)paged->page_size) : 0;
+  p.pages_per_seq = is_paged ? paged->pages_per_seq : 0;
+  p.num_pages = is_paged ? paged->num_pages : 0;
   char* ws = static_cast<char*>(desc->workspace);
   p.counters = reinterpret_cast<int*>(ws);
   p.ws_lse = reinterpret_cast<float*>(ws + pl.ws_lse_off);
@@ -1348,7 +1432,7 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();  // clear a stale error from unrelated work
-  launch_for(desc->dtype, desc->D, tree, p, pl, s, desc);
+  launch_for(desc->dtype, desc->D, tree, is_paged, p, pl, s, desc);
   if (hipGetLastError() != hipSuccess) return SPECMOE_ERR_LAUNCH;
   return SPECMOE_OK;
 }
@@ -1400,6 +1484,9 @@ const char* specmoe_status_str(int status) {
     case SPECMOE_ERR_SCALE: return "scale is not finite";
     case SPECMOE_ERR_LAUNCH: return "HIP kernel launch failed";
     case SPECMOE_ERR_MASK: return "draft masks hold at most 64 draft tokens: C_max must be <= 64";
+    case SPECMOE_ERR_PAGES:
+      return "page_size must be a power of two in [8, 65536], pages_per_seq and num_pages positive, "
+             "S_max = page_size * pages_per_seq";
     default: return "unknown status";
   }
 }
@@ -1414,6 +1501,15 @@ int specmoe_verify_attn_tree(const void* q, const void* k_cache, const void* v_c
                              const int32_t* chunk_lens, const uint64_t* draft_mask, float scale, float* out,
                              float* lse, void* stream, const specmoe_verify_desc* desc) {
   return run(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, true, scale, out, lse, stream, desc);
+}
+
+int specmoe_verify_attn_paged(const void* q, const void* k_pages, const void* v_pages, const int32_t* block_table,
+                              const int32_t* ctx_lens, const int32_t* chunk_lens, const uint64_t* draft_mask,
+                              float scale, float* out, float* lse, void* stream, const specmoe_verify_desc* desc,
+                              const specmoe_paged_kv* paged) {
+  if (!paged) return SPECMOE_ERR_NULL_POINTER;
+  return run(q, k_pages, v_pages, ctx_lens, chunk_lens, draft_mask, draft_mask != nullptr, scale, out, lse, stream,
+             desc, block_table, paged);
 }
 
 }  // extern "C"
