@@ -16,6 +16,13 @@
  * Section 3.1 "Model").  The KV cache is the paper's 4-D [b, h, s, d] layout
  * (Section 5.2, "CPU/GPU separation for Draft Model Execution").
  *
+ * Entry points: specmoe_verify_attn (chain drafts, the mask above),
+ * specmoe_verify_attn_tree (tree drafts: the draft part of the mask given as
+ * one bit word per draft token), specmoe_verify_attn_paged (either, over a
+ * paged KV cache).  q, k and v may be float32, bfloat16 or float16 (the
+ * paper's KV precision, Section 3.3).  The acceptance step that follows
+ * verification is in specmoe_accept.h.
+ *
  * All functions are plain C; every pointer named "device" is a HIP device
  * pointer, every other pointer is a host pointer.
  */

@@ -2,7 +2,10 @@
 //
 // Computes, for every sequence b and KV head, softmax(scale*Q K^T + M) V over
 // the cached context plus the draft chunk, with a chain mask inside the chunk
-// (SpecMoEOff, Section 5.1), and the log-sum-exp of every row.
+// or, for tree drafts, per-token draft-mask words (SpecMoEOff, Section 5.1,
+// Section 2.3), and the log-sum-exp of every row.  The KV cache is one slab
+// per sequence or a pool of pages found through a block table; elements are
+// f32, bf16 or f16.
 //
 // Design (one kernel launch per call, one persistent workgroup per CU):
 //   * Unit of work = (sequence b, KV head).  The c_b draft tokens times the g
