@@ -139,3 +139,38 @@ def test_paged_geometry_errors():
     out, _ = pkg.verify_attn_paged(q, kp, kp, torch.zeros((1, 4), dtype=torch.int32, device=d), lens, lens, 0.1)
     torch.cuda.synchronize()
     assert torch.isfinite(out[0, 0]).all()
+
+
+def test_batches_past_one_launch():
+    """More than 1024 sequences run as consecutive launches on the stream; the
+    lengths, draft masks and block tables of every launch are offset to its
+    sequences.  Chain, tree and paged calls on one batch of 1100 short
+    sequences, every row against the oracle."""
+    B, C = 1100, 4
+    rng = np.random.default_rng(81)
+    ctx = rng.integers(0, 200, B).astype(np.int32)
+    chunk = rng.integers(0, C + 1, B).astype(np.int32)
+    inp = _custom(B, 8, 2, 64, "bf16", ctx, chunk, C, seed=12)
+    words = wl.random_draft_masks(rng, chunk, C, density=0.6)
+    note("case 1100 sequences: chain, tree, paged")
+    d = dev()
+    q, k, v = to_dev(inp["q"], "bf16"), to_dev(inp["k_cache"], "bf16"), to_dev(inp["v_cache"], "bf16")
+    for mode in ("chain", "tree", "paged"):
+        out, lse = nan_outputs(*inp["q"].shape)
+        if mode == "chain":
+            pkg.verify_attn(q, k, v, i32(ctx), i32(chunk), inp["scale"], out=out, lse=lse)
+            ref = verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], ctx, chunk, inp["scale"], "bf16")
+        elif mode == "tree":
+            pkg.verify_attn_tree(q, k, v, i32(ctx), i32(chunk), torch.from_numpy(words.view(np.int64)).to(d),
+                                 inp["scale"], out=out, lse=lse)
+            ref = verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], ctx, chunk, inp["scale"], "bf16",
+                                  draft_mask=words)
+        else:
+            kp, table = wl.paginate(inp["k_cache"], 16, 4, wl.BF16_NAN)
+            vp, _ = wl.paginate(inp["v_cache"], 16, 4, wl.BF16_NAN)
+            pkg.verify_attn_paged(q, to_dev(kp, "bf16"), to_dev(vp, "bf16"), i32(table), i32(ctx), i32(chunk),
+                                  inp["scale"], out=out, lse=lse)
+            ref = verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], ctx, chunk, inp["scale"], "bf16")
+        torch.cuda.synchronize()
+        compare(out.cpu().double().numpy(), lse.cpu().double().numpy(), ref[0], ref[1], "bf16",
+                f"1100 sequences, {mode}")
