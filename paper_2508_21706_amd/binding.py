@@ -70,7 +70,7 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     p = path or LIB_PATH
     if not os.path.exists(p):
         raise RuntimeError(
-            f"{p} is missing: build the HIP library first (python -c 'import __graft_entry__ as g; g.build()')")
+            f"{p} is missing: build the HIP library first (python paper_2508_21706_amd/build.py)")
     lib = ctypes.CDLL(p)
     lib.specmoe_verify_attn.restype = ctypes.c_int
     lib.specmoe_verify_attn.argtypes = [
