@@ -396,9 +396,37 @@ def pin_tree_all_ones_is_bidirectional(m):
             np.testing.assert_allclose(o[b, : chunk[b], h], ref, rtol=0, atol=1e-12)
 
 
+def pin_split_and_combine(m):
+    """Attention over two complementary key sets, combined with log-sum-exp
+    weights (lse = logaddexp of the parts, out = sum of exp(lse_part - lse) *
+    out_part), equals attention over all keys: the merge the GPU applies to
+    the pieces of a split key range (Section 5.2 notes that a sequence split
+    needs this combine).  A part in which a row sees no key (lse -inf) drops
+    out."""
+    rng = np.random.default_rng(26)
+    n, l, d = 4, 11, 8
+    Q = rng.standard_normal((n, d))
+    K = rng.standard_normal((l + n, d))
+    V = rng.standard_normal((l + n, d))
+    M = m.chain_mask(l, n)
+    o, s = m.chunked_attention(Q, K, V, M, 0.7)
+    for cut in (1, 5, l, l + 2):
+        first = np.full_like(M, -np.inf)
+        second = np.full_like(M, -np.inf)
+        first[:, :cut] = M[:, :cut]
+        second[:, cut:] = M[:, cut:]
+        o1, s1 = m.chunked_attention(Q, K, V, first, 0.7)
+        o2, s2 = m.chunked_attention(Q, K, V, second, 0.7)
+        lse = np.logaddexp(s1, s2)
+        w1 = np.where(np.isfinite(s1), np.exp(s1 - lse), 0.0)[:, None]
+        w2 = np.where(np.isfinite(s2), np.exp(s2 - lse), 0.0)[:, None]
+        np.testing.assert_allclose(lse, s, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(w1 * o1 + w2 * o2, o, rtol=0, atol=1e-12)
+
+
 PINS = [pin_bf16_decoding, pin_f16_decoding, pin_f16_path, pin_hand_example, pin_uniform_closed_form, pin_decode_is_sdpa,
         pin_chunk_is_causal_prefill, pin_sequential_decode, pin_gqa_is_repeated_mha,
-        pin_invariants, pin_one_hot, pin_padding_and_poison, pin_bf16_path,
+        pin_invariants, pin_one_hot, pin_padding_and_poison, pin_bf16_path, pin_split_and_combine,
         pin_tree_chain_words_are_causal, pin_tree_row_is_its_root_path, pin_tree_matches_sdpa_boolean_mask,
         pin_tree_uniform_closed_form, pin_tree_all_ones_is_bidirectional]
 
