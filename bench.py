@@ -357,7 +357,9 @@ def main():
                      "traffic_over_algorithmic": round(traffic / launch_bytes, 4) if traffic else None,
                      "algorithmic_bytes_per_launch": launch_bytes,
                      "avg_launch_us": round(launch_s * 1e6, 3),
-                     "event_bracketed_launch_us": round(main_avg_ms * 1e3, 3)},
+                     "event_bracketed_launch_us": round(main_avg_ms * 1e3, 3),
+                     "event_bracketed_launch_us_p10_p50_p90": [round(float(np.percentile(main_ms, q_)) * 1e3, 3)
+                                                              for q_ in (10, 50, 90)]},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
