@@ -142,9 +142,105 @@ def pin_invariants(m):
         assert r["new_ctx_lens"][b] == inp["ctx_lens"][b] + a + 1
 
 
+# ------------------------------------------------------------- tree drafts
+
+def _tree_words(parents):
+    """Root-path words of a tree given by parent indices (parents[0] = -1)."""
+    words = []
+    for i, par in enumerate(parents):
+        words.append((1 << i) | (words[par] if par >= 0 else 0))
+    return words
+
+
+def pin_tree_chain_is_greedy(m):
+    """Chain words make tree acceptance the chain acceptance, with the path
+    of the first a + 1 tokens."""
+    w = wl.AcceptWorkload("t", 37, B=12, C_max=6, V=53, dtype="f32", accept_prob=0.8, description="")
+    chunk = np.random.default_rng(37).integers(0, 7, size=12)
+    inp = wl.make_accept_inputs(w, chunk_lens=chunk)
+    words = np.zeros((12, 6), np.uint64)
+    for b in range(12):
+        words[b, : chunk[b]] = [(1 << (i + 1)) - 1 for i in range(int(chunk[b]))]
+    r1 = m.accept_greedy_ref(inp["logits"], inp["tokens"], inp["ctx_lens"], chunk, "f32")
+    r2 = m.accept_tree_ref(inp["logits"], inp["tokens"], words, inp["ctx_lens"], chunk, "f32")
+    for key in r1:
+        assert np.array_equal(r1[key], r2[key]), key
+    for b in range(12):
+        want = (1 << (int(r1["accepted"][b]) + 1)) - 1 if chunk[b] else 0
+        assert int(r2["path"][b]) == want
+
+
+def pin_tree_known_branches(m):
+    """Root 0; 1 and 2 under 0; 3 under 1; 4 under 2; 5 under 4.  Node 1
+    misses, node 2 matches, node 3 matches its (rejected) parent's
+    prediction, node 4 matches, node 5 misses: the path is 0-2-4."""
+    rng = np.random.default_rng(38)
+    x, best = _known_rows(rng, 1, 6, 40)
+    words = np.array([_tree_words([-1, 0, 0, 1, 2, 4])], np.uint64)
+    tok = np.zeros((1, 6), np.int32)
+    tok[0, 1] = (best[0, 0] + 1) % 40
+    tok[0, 2] = best[0, 0]
+    tok[0, 3] = best[0, 1]
+    tok[0, 4] = best[0, 2]
+    tok[0, 5] = (best[0, 4] + 3) % 40
+    r = m.accept_tree_ref(x, tok, words, np.array([10]), np.array([6]), "f32")
+    assert int(r["path"][0]) == 0b10101 and r["accepted"][0] == 2
+    assert r["next_token"][0] == best[0, 4] and r["new_ctx_lens"][0] == 13
+
+
+def pin_tree_ties_take_lowest_index(m):
+    """Two equally deep accepted nodes (siblings 1 and 2 carry the same
+    token): the lower index wins; a deeper node beats both."""
+    rng = np.random.default_rng(39)
+    x, best = _known_rows(rng, 2, 4, 30)
+    words = np.array([_tree_words([-1, 0, 0, 2]), _tree_words([-1, 0, 0, 2])], np.uint64)
+    tok = np.zeros((2, 4), np.int32)
+    tok[:, 1] = best[:, 0]
+    tok[:, 2] = best[:, 0]
+    tok[0, 3] = (best[0, 2] + 1) % 30      # node 3 (under 2) misses: depth-1 tie, node 1 wins
+    tok[1, 3] = best[1, 2]                  # node 3 matches: depth 2 through node 2
+    r = m.accept_tree_ref(x, tok, words, np.array([0, 0]), np.array([4, 4]), "f32")
+    assert int(r["path"][0]) == 0b11 and r["next_token"][0] == best[0, 1]
+    assert int(r["path"][1]) == 0b1101 and r["accepted"][1] == 2 and r["next_token"][1] == best[1, 3]
+
+
+def pin_compaction_makes_the_path_a_chain(m):
+    """After compaction, chain attention over the context plus the accepted
+    path equals the tree attention of the path's nodes (the path's K/V rows
+    are what its nodes attended to)."""
+    from oracle import reference as ref
+    rng = np.random.default_rng(40)
+    B, Hq, Hkv, D, C = 2, 4, 2, 8, 6
+    ctx = np.array([7, 3], np.int32)
+    chunk = np.array([6, 5], np.int32)
+    S = 16
+    q = rng.standard_normal((B, C, Hq, D)).astype(np.float32)
+    k = rng.standard_normal((B, Hkv, S, D)).astype(np.float32)
+    v = rng.standard_normal((B, Hkv, S, D)).astype(np.float32)
+    words = np.zeros((B, C), np.uint64)
+    words[0, :6] = _tree_words([-1, 0, 0, 1, 2, 4])
+    words[1, :5] = _tree_words([-1, 0, 1, 0, 3])
+    paths = [0b10101, 0b11001]
+    o_t, s_t = ref.verify_attn_ref(q, k, v, ctx, chunk, 0.4, "f32", draft_mask=words)
+    kc = m.compact_path_ref(k, ctx, paths)
+    vc = m.compact_path_ref(v, ctx, paths)
+    for b in range(B):
+        nodes = [i for i in range(C) if (paths[b] >> i) & 1]
+        qp = np.zeros((1, C, Hq, D), np.float32)
+        qp[0, : len(nodes)] = q[b, nodes]
+        o_c, s_c = ref.verify_attn_ref(qp, kc[b:b + 1], vc[b:b + 1], ctx[b:b + 1],
+                                       np.array([len(nodes)], np.int32), 0.4, "f32")
+        np.testing.assert_allclose(o_c[0, : len(nodes)], o_t[b, nodes], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(s_c[0, : len(nodes)], s_t[b, nodes], rtol=0, atol=1e-12)
+        # rows outside the moved range keep their values
+        assert np.array_equal(kc[b, :, : ctx[b]], k[b, :, : ctx[b]])
+        assert np.array_equal(kc[b, :, ctx[b] + len(nodes):], k[b, :, ctx[b] + len(nodes):])
+
+
 PINS = [pin_known_acceptance_lengths, pin_rejection_stops_acceptance, pin_ties_take_lowest_id,
         pin_chunk_of_one_is_greedy_decoding, pin_empty_chunk_takes_no_step, pin_all_accepted,
-        pin_bf16_decodes_to_f32, pin_invariants]
+        pin_bf16_decodes_to_f32, pin_invariants, pin_tree_chain_is_greedy, pin_tree_known_branches,
+        pin_tree_ties_take_lowest_index, pin_compaction_makes_the_path_a_chain]
 
 
 @pytest.mark.parametrize("pin", PINS, ids=lambda p: p.__name__)
@@ -158,6 +254,10 @@ MUTATIONS = {
     "ctx_without_bonus": ("new_ctx[b] = int(ctx_lens[b]) + a + 1", "new_ctx[b] = int(ctx_lens[b]) + a"),
     "next_after_prediction": ("next_token[b] = argmax[b, a]", "next_token[b] = argmax[b, min(a + 1, c - 1)]"),
     "accepts_one_more": ("while a < c - 1 and", "while a < c and a < C_max - 1 and"),
+    "tree_parent_lowest_bit": ("    return rest.bit_length() - 1", "    return (rest & -rest).bit_length() - 1"),
+    "tree_ignores_parent": ("ok[i] = ok[par] and argmax[b, par]", "ok[i] = argmax[b, par]"),
+    "tree_ties_highest": ("key=lambda i: (depth[i], -i)", "key=lambda i: (depth[i], i)"),
+    "compaction_reversed": ("for j, k in enumerate(nodes):", "for j, k in enumerate(nodes[::-1]):"),
     "keeps_going_after_reject": ("while a < c - 1 and argmax[b, a] == int(draft_tokens[b, a + 1]):\n            a += 1",
                                  "a = sum(int(argmax[b, i] == int(draft_tokens[b, i + 1])) for i in range(c - 1))"),
 }
