@@ -94,6 +94,55 @@ int specmoe_accept_greedy(const void* logits, const int32_t* tokens, const int32
                           int32_t* next_token, int32_t* new_ctx_lens, void* stream,
                           const specmoe_accept_desc* desc);
 
+/*
+ * specmoe_accept_greedy_tree -- greedy acceptance of tree drafts.
+ *
+ * The chunk's tokens are the nodes of a draft tree in topological order
+ * (Section 2.3: tree drafts are verified as a sequence plus a mask relating
+ * them): node 0 is the last accepted token, the root; the parents come from
+ * draft_mask, the root-path words of specmoe_verify_attn_tree (word i holds
+ * the bits of i and its ancestors; a precondition).  Node i >= 1 is accepted
+ * when its parent is and tokens[i] equals the prediction at the parent
+ * (argmax of the parent's logits, ties to the lowest id).  The deepest
+ * accepted node wins, the lowest index among equally deep ones; a_b is its
+ * depth, the next token the prediction at it, new_ctx_lens = l_b + a_b + 1.
+ *
+ *   draft_mask   uint64 [B, C_max], device, 8-byte aligned; C_max <= 64
+ *                (SPECMOE_ERR_MASK otherwise).
+ *   path         uint64 [B] out, device, 8-byte aligned: the accepted path's
+ *                node bits (the winning node's word; 0 when c_b = 0).
+ * Every other argument, the workspace and the errors are those of
+ * specmoe_accept_greedy.  Follow it with specmoe_compact_accepted_kv, with
+ * the context lengths from before the step, to move the path's K/V rows
+ * into place.
+ */
+int specmoe_accept_greedy_tree(const void* logits, const int32_t* tokens, const uint64_t* draft_mask,
+                               const int32_t* ctx_lens, const int32_t* chunk_lens, int32_t* argmax,
+                               int32_t* accepted, int32_t* next_token, int32_t* new_ctx_lens,
+                               uint64_t* path, void* stream, const specmoe_accept_desc* desc);
+
+/*
+ * specmoe_compact_accepted_kv -- move an accepted tree path's K/V rows to
+ * the rows right after the context (Section 4.2: the KV cache is updated
+ * from the verification result).
+ *
+ * For every sequence b and KV head, the rows l_b + k of the set bits k of
+ * path[b] (ascending) move to rows l_b + 0, 1, ...; all rows are read
+ * before any is written.  Rows past S_max are skipped.
+ *
+ *   k_cache, v_cache  [B, Hkv, S_max, D] of desc's dtype, device, 16-byte
+ *                aligned (a contiguous cache; desc->B, Hkv, D, S_max, dtype
+ *                are used, the rest of desc is ignored).
+ *   ctx_lens     int32 [B], device: l_b before the step (not the updated
+ *                lengths).
+ *   path         uint64 [B], device: as written by specmoe_accept_greedy_tree.
+ * Status: SPECMOE_OK, SPECMOE_ERR_NULL_POINTER, SPECMOE_ERR_DTYPE,
+ * SPECMOE_ERR_HEAD_DIM, SPECMOE_ERR_SHAPE, SPECMOE_ERR_ALIGN or
+ * SPECMOE_ERR_LAUNCH.  Asynchronous on `stream`; allocates nothing.
+ */
+int specmoe_compact_accepted_kv(void* k_cache, void* v_cache, const int32_t* ctx_lens,
+                                const uint64_t* path, void* stream, const specmoe_verify_desc* desc);
+
 /* Bytes of workspace specmoe_accept_greedy needs for `desc`; 0 for an
  * invalid descriptor. */
 size_t specmoe_accept_workspace_bytes(const specmoe_accept_desc* desc);

@@ -6,6 +6,7 @@
 of ``libspecmoe_verify.so`` through its C-ABI; ``workloads`` draws the seeded
 synthetic inputs.
 """
-from .binding import (AcceptDesc, Desc, SpecMoEError, accept_desc, accept_greedy,  # noqa: F401
+from .binding import (AcceptDesc, Desc, SpecMoEError, accept_desc, accept_greedy, accept_greedy_tree,  # noqa: F401
+                      compact_accepted_kv,
                       alloc_accept_workspace, alloc_workspace, desc_for, key_tile, load_library, make_desc,
                       status_str, verify_attn, verify_attn_paged, verify_attn_tree, workspace_bytes)

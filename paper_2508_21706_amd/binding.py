@@ -92,6 +92,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.specmoe_verify_attn_key_tile.argtypes = [ctypes.POINTER(Desc)]
     lib.specmoe_accept_greedy.restype = ctypes.c_int
     lib.specmoe_accept_greedy.argtypes = [ctypes.c_void_p] * 9 + [ctypes.POINTER(AcceptDesc)]
+    lib.specmoe_accept_greedy_tree.restype = ctypes.c_int
+    lib.specmoe_accept_greedy_tree.argtypes = [ctypes.c_void_p] * 11 + [ctypes.POINTER(AcceptDesc)]
+    lib.specmoe_compact_accepted_kv.restype = ctypes.c_int
+    lib.specmoe_compact_accepted_kv.argtypes = [ctypes.c_void_p] * 5 + [ctypes.POINTER(Desc)]
     lib.specmoe_accept_workspace_bytes.restype = ctypes.c_size_t
     lib.specmoe_accept_workspace_bytes.argtypes = [ctypes.POINTER(AcceptDesc)]
     lib.specmoe_accept_workspace_init.restype = ctypes.c_int
@@ -315,9 +319,49 @@ def alloc_accept_workspace(desc: AcceptDesc, device, stream: Optional[torch.cuda
     return ws
 
 
+def accept_greedy_tree(logits: torch.Tensor, tokens: torch.Tensor, draft_mask: torch.Tensor, ctx_lens: torch.Tensor,
+                       chunk_lens: torch.Tensor, out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None,
+                       split: int = 0, stream: Optional[torch.cuda.Stream] = None, in_place: bool = False):
+    """Greedy acceptance of tree drafts; see ``specmoe_accept_greedy_tree``
+    in ``include/specmoe_accept.h``.  As ``accept_greedy`` plus ``draft_mask``
+    (int64 [B, C_max] root-path words, C_max <= 64); the result also holds
+    ``path`` (int64 [B]: the accepted path's node bits).  Call
+    ``compact_accepted_kv`` with the context lengths from before the step to
+    move the path's K/V rows into place."""
+    B, C_max = tokens.shape
+    mdt = draft_mask.dtype if draft_mask.dtype in (torch.int64, torch.uint64) else torch.int64
+    _check(draft_mask, "draft_mask", (B, C_max), mdt)
+    if out is None:
+        out = {}
+    if "path" not in out:
+        out["path"] = torch.empty((B,), dtype=torch.int64, device=logits.device)
+    _check(out["path"], "path", (B,), torch.int64)
+    return accept_greedy(logits, tokens, ctx_lens, chunk_lens, out=out, workspace=workspace, split=split,
+                         stream=stream, in_place=in_place, _tree=(draft_mask, out["path"]))
+
+
+def compact_accepted_kv(k_cache: torch.Tensor, v_cache: torch.Tensor, ctx_lens: torch.Tensor, path: torch.Tensor,
+                        stream: Optional[torch.cuda.Stream] = None):
+    """Move each sequence's accepted tree path's K/V rows to the rows right
+    after its context (``specmoe_compact_accepted_kv``); ``ctx_lens`` are the
+    lengths from before the acceptance step."""
+    lib = load_library()
+    B, Hkv, S_max, D = k_cache.shape
+    _check(k_cache, "k_cache", (B, Hkv, S_max, D), k_cache.dtype)
+    _check(v_cache, "v_cache", (B, Hkv, S_max, D), k_cache.dtype)
+    _check(ctx_lens, "ctx_lens", (B,), torch.int32)
+    _check(path, "path", (B,), path.dtype if path.dtype in (torch.int64, torch.uint64) else torch.int64)
+    desc = make_desc(B, Hkv, Hkv, D, 1, S_max, _dtype_code(k_cache))
+    s = stream if stream is not None else torch.cuda.current_stream(k_cache.device)
+    st = lib.specmoe_compact_accepted_kv(k_cache.data_ptr(), v_cache.data_ptr(), ctx_lens.data_ptr(), path.data_ptr(),
+                                         s.cuda_stream, ctypes.byref(desc))
+    if st != 0:
+        raise SpecMoEError(st, status_str(st))
+
+
 def accept_greedy(logits: torch.Tensor, tokens: torch.Tensor, ctx_lens: torch.Tensor, chunk_lens: torch.Tensor,
                   out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None, split: int = 0,
-                  stream: Optional[torch.cuda.Stream] = None, in_place: bool = False):
+                  stream: Optional[torch.cuda.Stream] = None, in_place: bool = False, _tree=None):
     """Greedy acceptance after verification; see ``include/specmoe_accept.h``.
 
     logits [B, C_max, V] (bf16 or f32), tokens int32 [B, C_max], ctx_lens /
@@ -336,11 +380,12 @@ def accept_greedy(logits: torch.Tensor, tokens: torch.Tensor, ctx_lens: torch.Te
     _check(chunk_lens, "chunk_lens", (B,), torch.int32)
     dev = logits.device
     if out is None:
-        out = {"argmax": torch.empty((B, C_max), dtype=torch.int32, device=dev),
-               "accepted": torch.empty((B,), dtype=torch.int32, device=dev),
-               "next_token": torch.empty((B,), dtype=torch.int32, device=dev)}
-        if not in_place:
-            out["new_ctx_lens"] = torch.empty((B,), dtype=torch.int32, device=dev)
+        out = {}
+    for key, shape in (("argmax", (B, C_max)), ("accepted", (B,)), ("next_token", (B,))):
+        if key not in out:
+            out[key] = torch.empty(shape, dtype=torch.int32, device=dev)
+    if not in_place and "new_ctx_lens" not in out:
+        out["new_ctx_lens"] = torch.empty((B,), dtype=torch.int32, device=dev)
     if in_place:
         out["new_ctx_lens"] = ctx_lens
     _check(out["argmax"], "argmax", (B, C_max), torch.int32)
@@ -354,10 +399,17 @@ def accept_greedy(logits: torch.Tensor, tokens: torch.Tensor, ctx_lens: torch.Te
         workspace = alloc_accept_workspace(desc, dev, s)
     desc.workspace = workspace.data_ptr()
     desc.workspace_bytes = workspace.numel() * workspace.element_size()
-    st = lib.specmoe_accept_greedy(logits.data_ptr(), tokens.data_ptr(), ctx_lens.data_ptr(), chunk_lens.data_ptr(),
-                                   out["argmax"].data_ptr(), out["accepted"].data_ptr(),
-                                   out["next_token"].data_ptr(), out["new_ctx_lens"].data_ptr(), s.cuda_stream,
-                                   ctypes.byref(desc))
+    if _tree is None:
+        st = lib.specmoe_accept_greedy(logits.data_ptr(), tokens.data_ptr(), ctx_lens.data_ptr(),
+                                       chunk_lens.data_ptr(), out["argmax"].data_ptr(), out["accepted"].data_ptr(),
+                                       out["next_token"].data_ptr(), out["new_ctx_lens"].data_ptr(), s.cuda_stream,
+                                       ctypes.byref(desc))
+    else:
+        st = lib.specmoe_accept_greedy_tree(logits.data_ptr(), tokens.data_ptr(), _tree[0].data_ptr(),
+                                            ctx_lens.data_ptr(), chunk_lens.data_ptr(), out["argmax"].data_ptr(),
+                                            out["accepted"].data_ptr(), out["next_token"].data_ptr(),
+                                            out["new_ctx_lens"].data_ptr(), _tree[1].data_ptr(), s.cuda_stream,
+                                            ctypes.byref(desc))
     if st != 0:
         raise SpecMoEError(st, status_str(st))
     return out

@@ -66,6 +66,8 @@ struct Params {
   int N;            // items: B * C_max * S
   int q;            // items per wave range
   int grouped;      // count arrivals per workgroup (every workgroup range meets < kGroupSeqs sequences)
+  const uint64_t* draft_mask;   // tree drafts: [B][C_max] root-path words (NULL: chain drafts)
+  uint64_t* path;               // tree drafts: [B] the accepted path's node bits
 };
 
 // (v, i) beats (bv, bi): a larger value, or an equal one at a lower index.
@@ -123,6 +125,7 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void accept_kernel(Params p
           p.accepted[b] = 0;
           p.next_token[b] = -1;
           p.new_ctx[b] = p.ctx_lens[b];
+          if (p.draft_mask) p.path[b] = 0;
         }
       }
       continue;
@@ -183,7 +186,12 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void accept_kernel(Params p
     // so that it rides the wait for the segment stores: the context length
     // and the draft tokens of the first 64 chunk positions
     const int l_b = p.ctx_lens[b];
-    const int tok0 = lane < c - 1 ? p.tokens[(size_t)b * p.C_max + lane + 1] : -1;
+    // chains: the draft after position lane; trees: node lane's own token
+    // and root-path word
+    const bool tree = p.draft_mask != nullptr;
+    const int tok0 = tree ? (lane < c ? p.tokens[(size_t)b * p.C_max + lane] : -1)
+                          : (lane < c - 1 ? p.tokens[(size_t)b * p.C_max + lane + 1] : -1);
+    const uint64_t word0 = tree && lane < c ? p.draft_mask[(size_t)b * p.C_max + lane] : 0;
     // count this wave once its segments are stored
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     const int first = b * CS, last = b * CS + c * p.S - 1;   // the sequence's valid items
@@ -239,6 +247,31 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void accept_kernel(Params p
         pred = ri == INT_MAX ? -1 : ri;   // (a row of NaN elects nothing)
       }
       if (k < p.C_max) p.argmax[(size_t)b * p.C_max + k] = pred;
+      if (tree) {
+        // (C_max <= 64: one pass) node k's parent is its highest ancestor
+        // bit below k; the edge into k is rejected when k's token differs
+        // from the parent's prediction, and a node is accepted when no edge
+        // on its root path is.  The deepest accepted node wins, the lowest
+        // index among equally deep ones.
+        const uint64_t cmask = c >= 64 ? ~0ull : (1ull << c) - 1;
+        const uint64_t word = word0 & cmask;
+        const uint64_t above = word & ((1ull << k) - 1);
+        const int par = above ? 63 - __builtin_clzll(above) : -1;
+        const int ppred = __shfl(pred, par & 63);
+        const bool reject = k >= 1 && k < c && (par < 0 || tok != ppred);
+        const uint64_t rejected = __ballot(reject);
+        const bool ok = k < c && (word & rejected) == 0;
+        int key = ok ? ((__popcll(word) - 1) << 8) | (255 - k) : -1;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) key = max(key, __shfl_xor(key, off));
+        const int d = 255 - (key & 255);
+        a = key >> 8;
+        next = __shfl(pred, d);
+        const uint32_t path_lo = (uint32_t)__shfl((int)(uint32_t)word, d);
+        const uint32_t path_hi = (uint32_t)__shfl((int)(uint32_t)(word >> 32), d);
+        if (lane == 0) p.path[b] = ((uint64_t)path_hi << 32) | path_lo;
+        break;
+      }
       // draft k + 1 is rejected when it differs from prediction k
       const bool reject = k < c - 1 && tok != pred;
       const uint64_t m = __ballot(reject);
@@ -262,6 +295,47 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void accept_kernel(Params p
       __hip_atomic_store(p.counters + b, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);   // ready for the next call
     }
   }
+}
+
+// Move the accepted path's K (blockIdx.y = 0) or V (1) rows of one (sequence,
+// KV head) (blockIdx.x) to the rows right after the context: row l + node_j
+// to row l + j for the j-th set bit node_j of the path word.  Every row is
+// read before any is written, so overlapping moves are safe.
+constexpr int kCompactThreads = 256;
+constexpr int kCompactChunks = 8;   // 16-byte chunks per thread: 64 rows of up to 512 bytes
+
+__global__ __launch_bounds__(kCompactThreads) void compact_kernel(char* k, char* v, const int32_t* ctx_lens,
+                                                                 const uint64_t* path, int Hkv, int S_max,
+                                                                 int row_bytes) {
+  const int unit = blockIdx.x;
+  const int b = unit / Hkv;
+  char* slab = (blockIdx.y == 0 ? k : v) + (size_t)unit * S_max * row_bytes;
+  const int l = min(max(ctx_lens[b], 0), S_max);
+  const uint64_t w = path[b];
+  const int chunks = row_bytes / 16;
+  const int n = __popcll(w);
+  u32x4 buf[kCompactChunks];
+  int dst[kCompactChunks];
+#pragma unroll
+  for (int u = 0; u < kCompactChunks; ++u) {
+    const int t = threadIdx.x + u * kCompactThreads;
+    const int j = t / chunks;
+    dst[u] = -1;
+    if (j < n) {
+      uint64_t rest = w;   // the j-th set bit: clear j lowest set bits
+      for (int i = 0; i < j; ++i) rest &= rest - 1;
+      const int node = __builtin_ctzll(rest);
+      const int ch = t - j * chunks;
+      if (node != j && l + node < S_max) {
+        buf[u] = *reinterpret_cast<const u32x4*>(slab + (size_t)(l + node) * row_bytes + 16 * ch);
+        dst[u] = (l + j) * row_bytes + 16 * ch;
+      }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int u = 0; u < kCompactChunks; ++u)
+    if (dst[u] >= 0) *reinterpret_cast<u32x4*>(slab + dst[u]) = buf[u];
 }
 
 __global__ void zero_kernel(int* x, int n) {
@@ -316,33 +390,9 @@ Plan make_plan(const specmoe_accept_desc* d) {
 
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
-}  // namespace
-
-extern "C" {
-
-size_t specmoe_accept_workspace_bytes(const specmoe_accept_desc* desc) {
-  if (validate(desc) != SPECMOE_OK) return 0;
-  return make_plan(desc).bytes;
-}
-
-int specmoe_accept_workspace_init(void* workspace, size_t workspace_bytes, void* stream,
-                                  const specmoe_accept_desc* desc) {
-  const int st = validate(desc);
-  if (st != SPECMOE_OK) return st;
-  if (!workspace) return SPECMOE_ERR_NULL_POINTER;
-  if (!aligned16(workspace)) return SPECMOE_ERR_ALIGN;
-  const Plan pl = make_plan(desc);
-  if (workspace_bytes < pl.bytes) return SPECMOE_ERR_WORKSPACE;
-  const int n = (int)(pl.counter_bytes / sizeof(int));
-  (void)hipGetLastError();
-  hipLaunchKernelGGL(zero_kernel, dim3((n + 255) / 256), dim3(256), 0, static_cast<hipStream_t>(stream),
-                     static_cast<int*>(workspace), n);
-  return hipGetLastError() == hipSuccess ? SPECMOE_OK : SPECMOE_ERR_LAUNCH;
-}
-
-int specmoe_accept_greedy(const void* logits, const int32_t* tokens, const int32_t* ctx_lens,
-                          const int32_t* chunk_lens, int32_t* argmax, int32_t* accepted, int32_t* next_token,
-                          int32_t* new_ctx_lens, void* stream, const specmoe_accept_desc* desc) {
+int accept_run(const void* logits, const int32_t* tokens, const uint64_t* draft_mask, const int32_t* ctx_lens,
+               const int32_t* chunk_lens, int32_t* argmax, int32_t* accepted, int32_t* next_token,
+               int32_t* new_ctx_lens, uint64_t* path, void* stream, const specmoe_accept_desc* desc) {
   const int st = validate(desc);
   if (st != SPECMOE_OK) return st;
   if (desc->B == 0) return SPECMOE_OK;
@@ -375,6 +425,8 @@ int specmoe_accept_greedy(const void* logits, const int32_t* tokens, const int32
   p.N = pl.N;
   p.q = pl.q;
   p.grouped = pl.grouped;
+  p.draft_mask = draft_mask;
+  p.path = path;
   const unsigned grid = (unsigned)pl.groups;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();
@@ -382,6 +434,70 @@ int specmoe_accept_greedy(const void* logits, const int32_t* tokens, const int32
     hipLaunchKernelGGL(accept_kernel<true>, dim3(grid), dim3(kThreads), 0, s, p);
   else
     hipLaunchKernelGGL(accept_kernel<false>, dim3(grid), dim3(kThreads), 0, s, p);
+  return hipGetLastError() == hipSuccess ? SPECMOE_OK : SPECMOE_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t specmoe_accept_workspace_bytes(const specmoe_accept_desc* desc) {
+  if (validate(desc) != SPECMOE_OK) return 0;
+  return make_plan(desc).bytes;
+}
+
+int specmoe_accept_workspace_init(void* workspace, size_t workspace_bytes, void* stream,
+                                  const specmoe_accept_desc* desc) {
+  const int st = validate(desc);
+  if (st != SPECMOE_OK) return st;
+  if (!workspace) return SPECMOE_ERR_NULL_POINTER;
+  if (!aligned16(workspace)) return SPECMOE_ERR_ALIGN;
+  const Plan pl = make_plan(desc);
+  if (workspace_bytes < pl.bytes) return SPECMOE_ERR_WORKSPACE;
+  const int n = (int)(pl.counter_bytes / sizeof(int));
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(zero_kernel, dim3((n + 255) / 256), dim3(256), 0, static_cast<hipStream_t>(stream),
+                     static_cast<int*>(workspace), n);
+  return hipGetLastError() == hipSuccess ? SPECMOE_OK : SPECMOE_ERR_LAUNCH;
+}
+
+int specmoe_accept_greedy(const void* logits, const int32_t* tokens, const int32_t* ctx_lens,
+                          const int32_t* chunk_lens, int32_t* argmax, int32_t* accepted, int32_t* next_token,
+                          int32_t* new_ctx_lens, void* stream, const specmoe_accept_desc* desc) {
+  return accept_run(logits, tokens, nullptr, ctx_lens, chunk_lens, argmax, accepted, next_token, new_ctx_lens,
+                    nullptr, stream, desc);
+}
+
+int specmoe_accept_greedy_tree(const void* logits, const int32_t* tokens, const uint64_t* draft_mask,
+                               const int32_t* ctx_lens, const int32_t* chunk_lens, int32_t* argmax,
+                               int32_t* accepted, int32_t* next_token, int32_t* new_ctx_lens, uint64_t* path,
+                               void* stream, const specmoe_accept_desc* desc) {
+  if (desc && validate(desc) == SPECMOE_OK && desc->C_max > 64) return SPECMOE_ERR_MASK;
+  if (desc && desc->B > 0 && (!draft_mask || !path)) return SPECMOE_ERR_NULL_POINTER;
+  if ((reinterpret_cast<uintptr_t>(draft_mask) & 7u) || (reinterpret_cast<uintptr_t>(path) & 7u))
+    return SPECMOE_ERR_ALIGN;
+  return accept_run(logits, tokens, draft_mask, ctx_lens, chunk_lens, argmax, accepted, next_token, new_ctx_lens,
+                    path, stream, desc);
+}
+
+int specmoe_compact_accepted_kv(void* k_cache, void* v_cache, const int32_t* ctx_lens, const uint64_t* path,
+                                void* stream, const specmoe_verify_desc* desc) {
+  if (!desc) return SPECMOE_ERR_NULL_POINTER;
+  if (desc->dtype != SPECMOE_F32 && desc->dtype != SPECMOE_BF16 && desc->dtype != SPECMOE_F16)
+    return SPECMOE_ERR_DTYPE;
+  if (desc->D != 64 && desc->D != 128) return SPECMOE_ERR_HEAD_DIM;
+  if (desc->B < 0 || desc->Hkv <= 0 || desc->S_max < 1) return SPECMOE_ERR_SHAPE;
+  const int64_t row_bytes = (int64_t)desc->D * (desc->dtype == SPECMOE_F32 ? 4 : 2);
+  if ((int64_t)desc->S_max * row_bytes >= ((int64_t)1 << 31) || (int64_t)desc->B * desc->Hkv >= (1 << 30))
+    return SPECMOE_ERR_SHAPE;
+  if (desc->B == 0) return SPECMOE_OK;
+  if (!k_cache || !v_cache || !ctx_lens || !path) return SPECMOE_ERR_NULL_POINTER;
+  if (!aligned16(k_cache) || !aligned16(v_cache) || (reinterpret_cast<uintptr_t>(path) & 7u))
+    return SPECMOE_ERR_ALIGN;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(compact_kernel, dim3(desc->B * desc->Hkv, 2), dim3(kCompactThreads), 0,
+                     static_cast<hipStream_t>(stream), static_cast<char*>(k_cache), static_cast<char*>(v_cache),
+                     ctx_lens, path, desc->Hkv, desc->S_max, (int)row_bytes);
   return hipGetLastError() == hipSuccess ? SPECMOE_OK : SPECMOE_ERR_LAUNCH;
 }
 

@@ -228,3 +228,31 @@ def test_accept_host_checks_and_workspace(lib):
     assert init(None, need, None, ctypes.byref(_adesc())) == -1
     assert init(FAKE, need - 1, None, ctypes.byref(_adesc())) == -8
     assert init(FAKE + 4, need, None, ctypes.byref(_adesc())) == -9
+
+
+def test_tree_acceptance_and_compaction_host_checks(lib):
+    d = _adesc(C_max=65)
+    d.workspace, d.workspace_bytes = FAKE, 1 << 30
+    assert lib.specmoe_accept_greedy_tree(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                                          ctypes.byref(d)) == -13
+    d = _adesc(C_max=16)
+    d.workspace, d.workspace_bytes = FAKE, 1 << 30
+    for i in (2, 9):   # draft_mask, path
+        args = [FAKE] * 11
+        args[i] = None
+        args[10] = None
+        assert lib.specmoe_accept_greedy_tree(*args, ctypes.byref(d)) == -1
+    args = [FAKE] * 10 + [None]
+    args[2] = FAKE + 4
+    assert lib.specmoe_accept_greedy_tree(*args, ctypes.byref(d)) == -9
+    compact = lib.specmoe_compact_accepted_kv
+    vd = _desc()
+    assert compact(FAKE, FAKE, FAKE, FAKE, None, None) == -1
+    assert compact(None, FAKE, FAKE, FAKE, None, ctypes.byref(vd)) == -1
+    assert compact(FAKE, FAKE, FAKE, None, None, ctypes.byref(vd)) == -1
+    assert compact(FAKE + 4, FAKE, FAKE, FAKE, None, ctypes.byref(vd)) == -9
+    assert compact(FAKE, FAKE, FAKE, FAKE + 4, None, ctypes.byref(vd)) == -9
+    assert compact(FAKE, FAKE, FAKE, FAKE, None, ctypes.byref(_desc(dtype=5))) == -5
+    assert compact(FAKE, FAKE, FAKE, FAKE, None, ctypes.byref(_desc(D=96))) == -4
+    assert compact(None, None, None, None, None, ctypes.byref(_desc(B=0))) == 0
+

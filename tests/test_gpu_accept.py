@@ -25,8 +25,9 @@ def note(msg):
 
 
 def logits_dev(x, dtype):
-    if dtype == "bf16":
-        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev())
+    if dtype in ("bf16", "f16"):
+        t16 = torch.bfloat16 if dtype == "bf16" else torch.float16
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(t16).to(dev())
     return torch.from_numpy(np.ascontiguousarray(x, np.float32)).to(dev())
 
 
@@ -150,3 +151,103 @@ def test_accept_many_short_sequences(B, C, V):
     inp = wl.make_accept_inputs(w, chunk_lens=chunk)
     for split in (0, 512):
         check(inp["logits"], inp["tokens"], inp["ctx_lens"], chunk, "bf16", f"short sequences B={B} C={C}", split)
+
+
+# ------------------------------------------------------------- tree drafts
+
+def _tree_case(seed, B, C, V, dtype, p_hit=0.75):
+    """Random recursive trees with planted predictions; node i's token is its
+    parent's planted prediction with probability p_hit."""
+    from oracle import tree_parent
+    w = wl.AcceptWorkload("tree", seed, B=B, C_max=C, V=V, dtype=dtype, accept_prob=0.0, description="")
+    rng = np.random.default_rng(seed)
+    chunk = rng.integers(0, C + 1, size=B).astype(np.int32)
+    chunk[: max(1, B // 4)] = C
+    inp = wl.make_accept_inputs(w, chunk_lens=chunk)
+    words = wl.tree_draft_masks(seed, chunk, C)
+    tokens = inp["tokens"].copy()
+    for b in range(B):
+        for i in range(1, int(chunk[b])):
+            par = tree_parent(words[b], i)
+            tokens[b, i] = inp["planted"][b, par] if rng.random() < p_hit else (inp["planted"][b, par] + 7) % V
+    return inp, tokens, words, chunk
+
+
+def run_tree(inp, tokens, words, chunk, dtype, split=0):
+    d = dev()
+    B, C = tokens.shape
+    out = {k: torch.full(s, -7, dtype=torch.int32, device=d)
+           for k, s in (("argmax", (B, C)), ("accepted", (B,)), ("next_token", (B,)), ("new_ctx_lens", (B,)))}
+    out["path"] = torch.full((B,), -7, dtype=torch.int64, device=d)
+    pkg.accept_greedy_tree(logits_dev(inp["logits"], dtype), i32(tokens), torch.from_numpy(words.view(np.int64)).to(d),
+                           i32(inp["ctx_lens"]), i32(chunk), out=out, split=split)
+    torch.cuda.synchronize()
+    return {k: v.cpu().numpy().astype(np.int64) for k, v in out.items()}
+
+
+@pytest.mark.parametrize("B,C,V,dtype", [(64, 16, 32000, "bf16"), (40, 64, 4096, "f32"), (300, 5, 2048, "bf16"),
+                                         (7, 1, 1024, "f32")])
+def test_accept_tree_matches_oracle(B, C, V, dtype):
+    from oracle import accept_tree_ref
+    inp, tokens, words, chunk = _tree_case(70 + C, B, C, V, dtype)
+    ref = accept_tree_ref(inp["logits"], tokens, words, inp["ctx_lens"], chunk, dtype)
+    for split in (0, 512):
+        note(f"case tree acceptance B={B} C={C} V={V} {dtype} split={split}")
+        got = run_tree(inp, tokens, words, chunk, dtype, split)
+        for k in ("argmax", "accepted", "next_token", "new_ctx_lens"):
+            assert np.array_equal(got[k], ref[k]), (k, np.argwhere(got[k] != ref[k])[:5])
+        assert [int(x) & ((1 << 64) - 1) for x in got["path"]] == [int(x) for x in ref["path"]]
+    note(f"[tree acceptance] accepted histogram {np.bincount(ref['accepted']).tolist()}")
+
+
+def test_accept_tree_chain_words_equal_chain_call():
+    w = dataclasses.replace(wl.ACCEPT_BY_NAME["accept_mixtral_b64"], B=20, V=4096)
+    chunk = np.random.default_rng(5).integers(0, w.C_max + 1, size=20).astype(np.int32)
+    inp = wl.make_accept_inputs(w, chunk_lens=chunk)
+    words = np.zeros((20, w.C_max), np.uint64)
+    for b in range(20):
+        words[b, : chunk[b]] = [(1 << (i + 1)) - 1 for i in range(int(chunk[b]))]
+    # chain tokens: draft i + 1 follows position i; tree tokens: node i's own
+    chain = run_accept(inp["logits"], inp["tokens"], inp["ctx_lens"], chunk, "bf16")
+    tree = run_tree(inp, inp["tokens"], words, chunk, "bf16")
+    for k in ("argmax", "accepted", "next_token", "new_ctx_lens"):
+        assert np.array_equal(chain[k], tree[k]), k
+
+
+@pytest.mark.parametrize("dtype,D", [("bf16", 128), ("f16", 64), ("f32", 128)])
+def test_compact_accepted_kv_matches_oracle(dtype, D):
+    """The accepted paths' K/V rows move after each context, overlapping
+    moves included; every other row keeps its value."""
+    from oracle import accept_tree_ref, compact_path_ref
+    d = dev()
+    B, Hkv, C = 9, 3, 12
+    inp, tokens, words, chunk = _tree_case(90, B, C, 2048, "f32", p_hit=0.9)
+    ref = accept_tree_ref(inp["logits"], tokens, words, inp["ctx_lens"], chunk, "f32")
+    ctx = np.random.default_rng(91).integers(0, 300, B).astype(np.int32)
+    S = 320
+    kv = [np.random.default_rng(92 + t).standard_normal((B, Hkv, S, D)).astype(np.float32) for t in range(2)]
+    enc = {"bf16": wl.f32_to_bf16_bits, "f16": wl.f32_to_f16_bits, "f32": lambda a: a}[dtype]
+    k_h, v_h = enc(kv[0]), enc(kv[1])
+    k_d = logits_dev(k_h, dtype) if dtype != "f32" else torch.from_numpy(k_h).to(d)
+    v_d = logits_dev(v_h, dtype) if dtype != "f32" else torch.from_numpy(v_h).to(d)
+    paths = np.array([int(x) for x in ref["path"]], dtype=np.uint64)
+    note(f"case compaction {dtype} D={D}")
+    pkg.compact_accepted_kv(k_d, v_d, i32(ctx), torch.from_numpy(paths.view(np.int64)).to(d))
+    torch.cuda.synchronize()
+    want_k = compact_path_ref(k_h, ctx, [int(x) for x in paths])
+    want_v = compact_path_ref(v_h, ctx, [int(x) for x in paths])
+    got_k = k_d.cpu().view(torch.int16).numpy().view(np.uint16) if dtype != "f32" else k_d.cpu().numpy()
+    got_v = v_d.cpu().view(torch.int16).numpy().view(np.uint16) if dtype != "f32" else v_d.cpu().numpy()
+    assert np.array_equal(got_k, want_k) and np.array_equal(got_v, want_v)
+    assert any(bin(int(x)).count("1") > 2 and int(x) != (1 << bin(int(x)).count("1")) - 1 for x in paths), \
+        "the case must hold paths with gaps"
+
+
+def test_accept_tree_rejects_wide_chunks():
+    d = dev()
+    x = torch.zeros((1, 65, 512), dtype=torch.bfloat16, device=d)
+    t = torch.zeros((1, 65), dtype=torch.int32, device=d)
+    n = torch.ones(1, dtype=torch.int32, device=d)
+    with pytest.raises(pkg.SpecMoEError) as e:
+        pkg.accept_greedy_tree(x, t, torch.zeros((1, 65), dtype=torch.int64, device=d), n, n)
+    assert e.value.status == -13
