@@ -124,8 +124,16 @@ def bench_accept(args):
     stream = torch.cuda.current_stream(dev)
     log(f"{n_sets} logits sets x {logit_bytes / 1e6:.1f} MB, {w.B} sequences x chunk {w.C_max}, vocabulary {w.V}")
 
+    mask_d = torch.from_numpy(inp["draft_mask"].view(np.int64)).to(dev) if w.tree else None
+    if w.tree:
+        out["path"] = torch.empty((w.B,), dtype=torch.int64, device=dev)
+
     def step(i):
-        pkg.accept_greedy(sets[i % n_sets], tokens, ctx, chunk_d, out=out, workspace=ws, stream=stream)
+        if w.tree:
+            pkg.accept_greedy_tree(sets[i % n_sets], tokens, mask_d, ctx, chunk_d, out=out, workspace=ws,
+                                   stream=stream)
+        else:
+            pkg.accept_greedy(sets[i % n_sets], tokens, ctx, chunk_d, out=out, workspace=ws, stream=stream)
 
     ms, settle_steps = run_timed(step, args, stream)
     t = ms / 1e3
@@ -134,12 +142,15 @@ def bench_accept(args):
     log(f"step {ms * 1e3:.2f} us -> {value:.0f} GB/s of logits, {w.B / t / 1e6:.2f} M sequence decisions/s")
     cpu = None
     if args.cpu_budget > 0:
-        from oracle import accept_greedy_ref
+        from oracle import accept_greedy_ref, accept_tree_ref
         log("timing the oracle on the host ...")
         passes, t_total = 0, 0.0
         while t_total < args.cpu_budget:
             t0 = time.perf_counter()
-            accept_greedy_ref(inp["logits"], inp["tokens"], inp["ctx_lens"], chunk, w.dtype)
+            if w.tree:
+                accept_tree_ref(inp["logits"], inp["tokens"], inp["draft_mask"], inp["ctx_lens"], chunk, w.dtype)
+            else:
+                accept_greedy_ref(inp["logits"], inp["tokens"], inp["ctx_lens"], chunk, w.dtype)
             t_total += time.perf_counter() - t0
             passes += 1
         cpu = {"value": passes * logit_bytes / t_total / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
@@ -151,6 +162,7 @@ def bench_accept(args):
         "warmup": args.warmup, "settle_steps": settle_steps, "ms_per_step": round(ms, 6),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": w.name, "description": w.description, "B": w.B, "C_max": w.C_max, "V": w.V,
+                   "tree": w.tree,
                    "input_sets": n_sets, "parallelism": "single GPU"},
         "sequence_decisions_per_s": round(w.B / t, 1),
         "roofline": {"bound": "hbm", "kernel": ACCEPT_KERNEL, "achieved": round(achieved, 2),

@@ -336,6 +336,7 @@ class AcceptWorkload:
     dtype: str            # "f32" or "bf16" logits
     accept_prob: float    # chance that a draft token equals the planted prediction
     description: str
+    tree: bool = False    # tree drafts: random recursive trees, tokens follow the parents' predictions
 
     @property
     def elt_bytes(self) -> int:
@@ -349,6 +350,9 @@ ACCEPT_WORKLOADS = [
     AcceptWorkload("accept_large_b256", 12, B=256, C_max=8, V=32000, dtype="bf16", accept_prob=0.7,
                    description="greedy acceptance after the B=256 verification: chunk 8, vocabulary 32000, "
                                "bf16 logits"),
+    AcceptWorkload("accept_tree_b64", 14, B=64, C_max=16, V=32000, dtype="bf16", accept_prob=0.7,
+                   description="greedy acceptance of 16-node tree drafts after the Mixtral B=64 verification: "
+                               "vocabulary 32000, bf16 logits", tree=True),
     AcceptWorkload("accept_tiny_f32", 13, B=3, C_max=4, V=1000, dtype="f32", accept_prob=0.6,
                    description="tiny f32 acceptance: B=3, chunk 4, vocabulary 1000"),
 ]
@@ -383,7 +387,18 @@ def make_accept_inputs(w: AcceptWorkload, chunk_lens=None, ctx_lens=None, fill: 
         x[b, chunk[b]:] = fill
         tokens[b, chunk[b]:] = -1
     logits = _encode(x, w.dtype)
-    return dict(logits=logits, tokens=tokens, ctx_lens=ctx, chunk_lens=chunk, planted=planted, workload=w)
+    words = None
+    if w.tree:
+        # tree drafts: node i's token is its parent's planted prediction with
+        # probability accept_prob (the parent is the highest ancestor bit of
+        # the node's root-path word below the node)
+        words = tree_draft_masks(w.index, chunk, C)
+        for b in range(B):
+            for i in range(1, int(chunk[b])):
+                par = (int(words[b, i]) & ~(1 << i)).bit_length() - 1
+                tokens[b, i] = planted[b, par] if hit[b, i] else other[b, par]
+    return dict(logits=logits, tokens=tokens, ctx_lens=ctx, chunk_lens=chunk, planted=planted, workload=w,
+                draft_mask=words)
 
 
 def algorithmic_kv_bytes(w: Workload, ctx_lens, chunk_lens) -> int:
