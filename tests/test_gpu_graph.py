@@ -39,16 +39,32 @@ def test_verify_and_accept_replay_in_a_graph():
             "next_token": torch.empty((aw.B,), dtype=torch.int32, device=d),
             "new_ctx_lens": torch.empty((aw.B,), dtype=torch.int32, device=d)}
 
+    # tree acceptance and the path compaction on a copy of the cache
+    words = wl.tree_draft_masks(7, inp["chunk_lens"], w.C_max)
+    mask = torch.from_numpy(words.view(np.int64)).to(d)
+    tout = {"argmax": torch.empty((aw.B, aw.C_max), dtype=torch.int32, device=d),
+            "accepted": torch.empty((aw.B,), dtype=torch.int32, device=d),
+            "next_token": torch.empty((aw.B,), dtype=torch.int32, device=d),
+            "new_ctx_lens": torch.empty((aw.B,), dtype=torch.int32, device=d),
+            "path": torch.empty((aw.B,), dtype=torch.int64, device=d)}
+    kc, vc = k.clone(), v.clone()
+
     def step(stream):
         pkg.verify_attn(q, k, v, ctx, chunk, w.scale, out=out, lse=lse, workspace=ws, grid_blocks=64,
                         stream=stream)
         pkg.accept_greedy(logits, tokens, ctx, chunk, out=aout, workspace=aws, stream=stream)
+        kc.copy_(k)
+        vc.copy_(v)
+        pkg.accept_greedy_tree(logits, tokens, mask, ctx, chunk, out=tout, workspace=aws, stream=stream)
+        pkg.compact_accepted_kv(kc, vc, ctx, tout["path"], stream=stream)
 
     # eager reference, checked against the oracles
     step(torch.cuda.current_stream(d))
     torch.cuda.synchronize()
     eager_o, eager_l = out.clone(), lse.clone()
     eager_a = {kk: vv.clone() for kk, vv in aout.items()}
+    eager_t = {kk: vv.clone() for kk, vv in tout.items()}
+    eager_kc, eager_vc = kc.clone(), vc.clone()
     ref_o, ref_l = verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], inp["ctx_lens"], inp["chunk_lens"],
                                    w.scale, "bf16")
     compare(eager_o.cpu().double().numpy(), eager_l.cpu().double().numpy(), ref_o, ref_l, "bf16", "graph eager")
@@ -76,12 +92,21 @@ def test_verify_and_accept_replay_in_a_graph():
         out.fill_(float("nan"))
         for t in aout.values():
             t.fill_(-9)
+        for t in tout.values():
+            t.fill_(-9)
+        kc.zero_()
+        vc.zero_()
         graph.replay()
         torch.cuda.synchronize()
         note(f"graph replay {rep}")
         assert torch.equal(out, eager_o) and torch.equal(lse, eager_l), f"replay {rep}: attention differs"
         for kk, vv in aout.items():
             assert torch.equal(vv, eager_a[kk]), f"replay {rep}: {kk} differs"
+        for kk, vv in tout.items():
+            assert torch.equal(vv, eager_t[kk]), f"replay {rep}: tree {kk} differs"
+        # bitwise (the caches hold NaN-poisoned rows past each sequence)
+        assert torch.equal(kc.view(torch.int16), eager_kc.view(torch.int16)) and \
+            torch.equal(vc.view(torch.int16), eager_vc.view(torch.int16)), f"replay {rep}: compaction differs"
     # the workspaces' counters are back to zero
     assert int(ws[: 1024 * w.Hkv * 4].view(torch.int32).abs().sum()) == 0
     assert int(aws[: 65536 * 4].view(torch.int32).abs().sum()) == 0
