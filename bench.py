@@ -229,9 +229,9 @@ def main():
                          "float32 write) 5 times: the known byte counts calibrate the HBM traffic counters")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on exactly one GPU: the verification-attention path has no "
-              "multi-GPU component in this build (see the sharding notes in the design doc).",
-              file=sys.stderr)
+        print("bench.py runs on exactly one GPU: the verification-attention kernel works on one "
+              "GPU's share of the batch and has no multi-GPU component; run one process per GPU "
+              "on disjoint sequences instead.", file=sys.stderr)
         sys.exit(2)
 
     import torch
