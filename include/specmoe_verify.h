@@ -59,14 +59,27 @@ enum {
   SPECMOE_ERR_WORKSPACE = -8,     /* workspace smaller than the size query returns    */
   SPECMOE_ERR_ALIGN = -9,         /* q, k_cache, v_cache, out or workspace is not
                                      16-byte aligned, or draft_mask not 8-byte aligned */
-  SPECMOE_ERR_SCALE = -10,        /* scale is not finite                              */
+  SPECMOE_ERR_SCALE = -10,        /* scale is not finite and positive                 */
   SPECMOE_ERR_LAUNCH = -11,       /* HIP reported an error for a kernel launch        */
-  SPECMOE_ERR_FLAGS = -12,        /* flags is not 0                                   */
+  SPECMOE_ERR_FLAGS = -12,        /* flags holds a bit other than SPECMOE_FLAG_NO_WAIT */
   SPECMOE_ERR_MASK = -13,         /* a draft mask with C_max > 64 (one 64-bit word per
                                      draft token covers at most 64 draft tokens)      */
-  SPECMOE_ERR_PAGES = -14         /* paged cache: page_size not a power of two in
+  SPECMOE_ERR_PAGES = -14,        /* paged cache: page_size not a power of two in
                                      [8, 65536], pages_per_seq or num_pages < 1, or
                                      S_max != page_size * pages_per_seq               */
+  SPECMOE_ERR_HANDOFF = -15       /* (specmoe_verify_attn_status) a kernel's wait for
+                                     another wave of its workgroup gave up: the
+                                     results of that call are unspecified            */
+};
+
+/* desc->flags bits. */
+enum {
+  /* Diagnostics only: every in-kernel wait for another wave gives up after a
+   * single check instead of polling for about 0.1 s.  The kernels still end
+   * normally and stay inside every buffer, but the results are unspecified
+   * and the workspace's status word records the give-up (see
+   * specmoe_verify_attn_status).  It exists to exercise that reporting. */
+  SPECMOE_FLAG_NO_WAIT = 1
 };
 
 /* Problem description.  Sizes are in elements unless stated otherwise. */
@@ -81,13 +94,10 @@ typedef struct specmoe_verify_desc {
   int32_t dtype;      /* specmoe_dtype of q, k_cache, v_cache                       */
   int32_t grid_blocks;  /* persistent workgroups that share the key tiles; 0 = the
                            library default (256: one per CU of an MI355X)          */
-  int32_t flags;        /* reserved, must be 0                                     */
+  int32_t flags;        /* 0, or SPECMOE_FLAG_NO_WAIT (diagnostics)                */
   void* workspace;          /* device; caller-allocated scratch, >= workspace_bytes,
-                               whose counter region is zero (see below)             */
+                               whose zeroed region is zero (see below)              */
   size_t workspace_bytes;   /* size of workspace in bytes                           */
-  void* ev_main_begin;      /* optional hipEvent_t recorded on the stream right
-                               before the main kernel (NULL: none)                  */
-  void* ev_main_end;        /* optional hipEvent_t recorded right after it          */
 } specmoe_verify_desc;
 
 /*
@@ -113,7 +123,8 @@ typedef struct specmoe_verify_desc {
  *              already appended.  Rows >= l_b + c_b are never read.
  *   ctx_lens   int32 [B]: l_b, the cached context length of sequence b.
  *   chunk_lens int32 [B]: c_b, the draft chunk length (gamma + 1) of b.
- *   scale      softmax scale applied to q.k (e.g. 1/sqrt(D)).
+ *   scale      softmax scale applied to q.k (e.g. 1/sqrt(D)); finite and > 0
+ *              (SPECMOE_ERR_SCALE otherwise).
  *   out        float32 [B, C_max, Hq, D]: attention output.
  *   lse        float32 [B, C_max, Hq]: natural-log log-sum-exp of the scaled,
  *              masked scores of each row.
@@ -138,7 +149,11 @@ typedef struct specmoe_verify_desc {
  *
  * Errors: all host-side checks run before any HIP call; on an error nothing
  * is enqueued and one of the SPECMOE_ERR_* codes is returned.  A launch
- * failure reported by HIP returns SPECMOE_ERR_LAUNCH.
+ * failure reported by HIP returns SPECMOE_ERR_LAUNCH.  The waves of a
+ * workgroup hand tiles to each other through bounded waits; a wait that
+ * gives up (never expected: it means a broken hand-off) cannot be seen by
+ * the asynchronous call itself, so it sets a sticky bit in the workspace,
+ * which specmoe_verify_attn_status reports.
  */
 int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
                         const int32_t* ctx_lens, const int32_t* chunk_lens,
@@ -218,23 +233,37 @@ int specmoe_verify_attn_paged(const void* q, const void* k_pages, const void* v_
 
 /* Bytes of device workspace specmoe_verify_attn needs for `desc` (its
  * grid_blocks included); 0 for an invalid descriptor.  The workspace starts
- * with a counter region -- one arrival counter per (sequence, KV head) of a
- * launch of up to 1024 sequences, at offsets that depend only on Hkv --
- * followed by the partial results of pieces (two slots per workgroup).  The
- * counter region must be zero before the first call; every call that
- * completes leaves it zero again (the piece that merges a unit resets the
- * unit's counter), so a workspace initialised once by
- * specmoe_verify_attn_workspace_init can be reused for any number of calls
- * with the same Hkv, any B, lengths and grid_blocks, as long as it is large
- * enough for them. */
+ * with a zeroed region -- a 256-byte header holding the sticky status word,
+ * then one arrival counter per (sequence, KV head) of a launch of up to 1024
+ * sequences, at offsets that depend only on Hkv -- followed by the partial
+ * results of pieces (two slots per workgroup).  The zeroed region must be
+ * zero before the first call; every call that completes leaves the counters
+ * zero again (the piece that merges a unit resets the unit's counter), so a
+ * workspace initialised once by specmoe_verify_attn_workspace_init can be
+ * reused for any number of calls with the same Hkv, any B, lengths and
+ * grid_blocks, as long as it is large enough for them. */
 size_t specmoe_verify_attn_workspace_bytes(const specmoe_verify_desc* desc);
 
-/* Zero the counter region of `workspace` (device, workspace_bytes long) with
- * a small kernel on `stream` (a hipStream_t; NULL: the null stream).  Status:
+/* Zero the zeroed region (status word and counters) of `workspace` (device,
+ * workspace_bytes long) with a small kernel on `stream` (a hipStream_t; NULL:
+ * the null stream); this also clears a recorded give-up.  Status:
  * SPECMOE_OK, a descriptor error, SPECMOE_ERR_NULL_POINTER, SPECMOE_ERR_ALIGN,
  * SPECMOE_ERR_WORKSPACE if the buffer is too small, or SPECMOE_ERR_LAUNCH. */
 int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, void* stream,
                                        const specmoe_verify_desc* desc);
+
+/* Status of the calls made so far with `workspace` (device, workspace_bytes
+ * long, 16-byte aligned): SPECMOE_ERR_HANDOFF if a kernel's wait for another
+ * wave gave up in any call since the workspace was last initialised, else
+ * SPECMOE_OK.  Copies the 4-byte status word to the host on `stream` (a
+ * hipStream_t; NULL: the null stream) and synchronises with that stream, so
+ * it reports every call enqueued on it before; the word stays set until
+ * specmoe_verify_attn_workspace_init clears it.  After SPECMOE_ERR_HANDOFF
+ * the workspace must be initialised again before its next call: a give-up
+ * can also leave arrival counters set.  SPECMOE_ERR_NULL_POINTER,
+ * SPECMOE_ERR_ALIGN, SPECMOE_ERR_WORKSPACE (fewer than 256 bytes) or
+ * SPECMOE_ERR_LAUNCH (HIP reported an error for the copy) otherwise. */
+int specmoe_verify_attn_status(const void* workspace, size_t workspace_bytes, void* stream);
 
 /* Keys per tile for `desc`'s dtype and D (32 KB of K rows).  Negative status
  * for an invalid dtype or D. */

@@ -24,8 +24,9 @@ STATUS = {
     0: "SPECMOE_OK", -1: "SPECMOE_ERR_NULL_POINTER", -2: "SPECMOE_ERR_SHAPE", -3: "SPECMOE_ERR_GQA",
     -4: "SPECMOE_ERR_HEAD_DIM", -5: "SPECMOE_ERR_DTYPE", -6: "SPECMOE_ERR_ROWS", -7: "SPECMOE_ERR_GRID",
     -8: "SPECMOE_ERR_WORKSPACE", -9: "SPECMOE_ERR_ALIGN", -10: "SPECMOE_ERR_SCALE", -11: "SPECMOE_ERR_LAUNCH",
-    -12: "SPECMOE_ERR_FLAGS", -13: "SPECMOE_ERR_MASK", -14: "SPECMOE_ERR_PAGES",
+    -12: "SPECMOE_ERR_FLAGS", -13: "SPECMOE_ERR_MASK", -14: "SPECMOE_ERR_PAGES", -15: "SPECMOE_ERR_HANDOFF",
 }
+SPECMOE_FLAG_NO_WAIT = 1
 
 
 class Desc(ctypes.Structure):
@@ -35,7 +36,6 @@ class Desc(ctypes.Structure):
         ("C_max", ctypes.c_int32), ("S_max", ctypes.c_int32), ("dtype", ctypes.c_int32),
         ("grid_blocks", ctypes.c_int32), ("flags", ctypes.c_int32),
         ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
-        ("ev_main_begin", ctypes.c_void_p), ("ev_main_end", ctypes.c_void_p),
     ]
 
 
@@ -88,6 +88,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.specmoe_verify_attn_workspace_init.restype = ctypes.c_int
     lib.specmoe_verify_attn_workspace_init.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                                        ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_status.restype = ctypes.c_int
+    lib.specmoe_verify_attn_status.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
     lib.specmoe_verify_attn_key_tile.restype = ctypes.c_int32
     lib.specmoe_verify_attn_key_tile.argtypes = [ctypes.POINTER(Desc)]
     lib.specmoe_accept_greedy.restype = ctypes.c_int
@@ -113,13 +115,11 @@ def status_str(status: int) -> str:
 
 
 def make_desc(B, Hq, Hkv, D, C_max, S_max, dtype: int, grid_blocks: int = 0, flags: int = 0,
-              workspace: Optional[torch.Tensor] = None, events=None) -> Desc:
-    d = Desc(B, Hq, Hkv, D, C_max, S_max, dtype, grid_blocks, flags, None, 0, None, None)
+              workspace: Optional[torch.Tensor] = None) -> Desc:
+    d = Desc(B, Hq, Hkv, D, C_max, S_max, dtype, grid_blocks, flags, None, 0)
     if workspace is not None:
         d.workspace = workspace.data_ptr()
         d.workspace_bytes = workspace.numel() * workspace.element_size()
-    if events is not None:
-        d.ev_main_begin, d.ev_main_end = events
     return d
 
 
@@ -148,16 +148,32 @@ def key_tile(desc: Desc) -> int:
 
 
 def alloc_workspace(desc: Desc, device, stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-    """Allocate a workspace for ``desc`` and zero its counters on the stream."""
+    """Allocate a workspace for ``desc`` and zero its status word and counters
+    on the stream.  The memory comes from the stream's own pool of the caching
+    allocator, so that when the tensor is dropped, the block is only reused by
+    work ordered after what was enqueued on that stream."""
     n = workspace_bytes(desc)
     if n == 0:
         raise SpecMoEError(-2, "invalid descriptor")
-    ws = torch.empty(n, dtype=torch.uint8, device=device)
     s = stream if stream is not None else torch.cuda.current_stream(device)
+    with torch.cuda.stream(s):
+        ws = torch.empty(n, dtype=torch.uint8, device=device)
     st = load_library().specmoe_verify_attn_workspace_init(ws.data_ptr(), n, s.cuda_stream, ctypes.byref(desc))
     if st != 0:
         raise SpecMoEError(st, status_str(st))
     return ws
+
+
+def workspace_status(workspace: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> int:
+    """``specmoe_verify_attn_status``: synchronises with the stream and returns
+    0 (SPECMOE_OK) or -15 (SPECMOE_ERR_HANDOFF: an in-kernel wait gave up in a
+    call since the workspace was initialised)."""
+    s = stream if stream is not None else torch.cuda.current_stream(workspace.device)
+    st = load_library().specmoe_verify_attn_status(workspace.data_ptr(),
+                                                    workspace.numel() * workspace.element_size(), s.cuda_stream)
+    if st not in (0, -15):
+        raise SpecMoEError(st, status_str(st))
+    return st
 
 
 def _check(t: torch.Tensor, name: str, shape, dtype):
@@ -175,7 +191,7 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                 ctx_lens: torch.Tensor, chunk_lens: torch.Tensor, scale: float,
                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
-                stream: Optional[torch.cuda.Stream] = None, events=None,
+                stream: Optional[torch.cuda.Stream] = None, flags: int = 0,
                 check_lengths: bool = False):
     """Chunked verification attention; see ``include/specmoe_verify.h``.
 
@@ -189,14 +205,14 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     grid give bitwise-identical results.
     """
     return _call(q, k_cache, v_cache, ctx_lens, chunk_lens, None, scale, out, lse, workspace, grid_blocks,
-                 stream, events, check_lengths)
+                 stream, flags, check_lengths)
 
 
 def verify_attn_tree(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                      ctx_lens: torch.Tensor, chunk_lens: torch.Tensor, draft_mask: torch.Tensor, scale: float,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                      workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
-                     stream: Optional[torch.cuda.Stream] = None, events=None,
+                     stream: Optional[torch.cuda.Stream] = None, flags: int = 0,
                      check_lengths: bool = False):
     """Chunked verification attention for tree drafts; see
     ``specmoe_verify_attn_tree`` in ``include/specmoe_verify.h``.
@@ -207,7 +223,7 @@ def verify_attn_tree(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tens
     C_max must be <= 64.
     """
     return _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse, workspace,
-                 grid_blocks, stream, events, check_lengths)
+                 grid_blocks, stream, flags, check_lengths)
 
 
 def verify_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Tensor, block_table: torch.Tensor,
@@ -215,7 +231,7 @@ def verify_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Ten
                       draft_mask: Optional[torch.Tensor] = None,
                       out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                       workspace: Optional[torch.Tensor] = None, grid_blocks: int = 0,
-                      stream: Optional[torch.cuda.Stream] = None, events=None,
+                      stream: Optional[torch.cuda.Stream] = None, flags: int = 0,
                       check_lengths: bool = False):
     """Chunked verification attention over a paged KV cache; see
     ``specmoe_verify_attn_paged`` in ``include/specmoe_verify.h``.
@@ -233,11 +249,11 @@ def verify_attn_paged(q: torch.Tensor, k_pages: torch.Tensor, v_pages: torch.Ten
     _check(block_table, "block_table", (q.shape[0], block_table.shape[1]), torch.int32)
     paged = PagedKV(page_size, block_table.shape[1], num_pages)
     return _call(q, k_pages, v_pages, ctx_lens, chunk_lens, draft_mask, scale, out, lse, workspace, grid_blocks,
-                 stream, events, check_lengths, paged=paged, block_table=block_table)
+                 stream, flags, check_lengths, paged=paged, block_table=block_table)
 
 
 def _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse, workspace, grid_blocks,
-          stream, events, check_lengths, paged: Optional[PagedKV] = None, block_table=None):
+          stream, flags, check_lengths, paged: Optional[PagedKV] = None, block_table=None):
     lib = load_library()
     B, C_max, Hq, D = q.shape
     if k_cache.dim() != 4:
@@ -263,22 +279,21 @@ def _call(q, k_cache, v_cache, ctx_lens, chunk_lens, draft_mask, scale, out, lse
         l = ctx_lens.cpu()
         if (c < 0).any() or (c > C_max).any() or (l < 0).any() or (l + c > S_max).any():
             raise ValueError("lengths break 0 <= c_b <= C_max, l_b >= 0, l_b + c_b <= S_max")
-    if out is None:
-        out = torch.empty((B, C_max, Hq, D), dtype=torch.float32, device=q.device)
-    if lse is None:
-        lse = torch.empty((B, C_max, Hq), dtype=torch.float32, device=q.device)
+    s = stream if stream is not None else torch.cuda.current_stream(q.device)
+    with torch.cuda.stream(s):   # outputs from the launch stream's pool
+        if out is None:
+            out = torch.empty((B, C_max, Hq, D), dtype=torch.float32, device=q.device)
+        if lse is None:
+            lse = torch.empty((B, C_max, Hq), dtype=torch.float32, device=q.device)
     _check(out, "out", (B, C_max, Hq, D), torch.float32)
     _check(lse, "lse", (B, C_max, Hq), torch.float32)
-    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks)
-    s = stream if stream is not None else torch.cuda.current_stream(q.device)
+    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks, flags)
     if B == 0:
         return out, lse
     if workspace is None:
         workspace = alloc_workspace(desc, q.device, s)
     desc.workspace = workspace.data_ptr()
     desc.workspace_bytes = workspace.numel() * workspace.element_size()
-    if events is not None:
-        desc.ev_main_begin, desc.ev_main_end = events
     if paged is not None:
         st = lib.specmoe_verify_attn_paged(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(),
                                            block_table.data_ptr(), ctx_lens.data_ptr(), chunk_lens.data_ptr(),
@@ -311,8 +326,9 @@ def alloc_accept_workspace(desc: AcceptDesc, device, stream: Optional[torch.cuda
     n = int(lib.specmoe_accept_workspace_bytes(ctypes.byref(desc)))
     if n == 0:
         raise SpecMoEError(-2, "invalid acceptance descriptor")
-    ws = torch.empty(n, dtype=torch.uint8, device=device)
     s = stream if stream is not None else torch.cuda.current_stream(device)
+    with torch.cuda.stream(s):   # from the stream's pool (see alloc_workspace)
+        ws = torch.empty(n, dtype=torch.uint8, device=device)
     st = lib.specmoe_accept_workspace_init(ws.data_ptr(), n, s.cuda_stream, ctypes.byref(desc))
     if st != 0:
         raise SpecMoEError(st, status_str(st))

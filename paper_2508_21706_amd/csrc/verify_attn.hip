@@ -115,6 +115,8 @@ struct Params {
   const int32_t* chunk_lens;
   float* out;
   float* lse;
+  int* status;      // sticky flags of the workspace: kGaveUp once an in-kernel wait gave up
+  int spin_limit;   // polls before an in-kernel wait gives up
   int* counters;    // [B*Hkv] pieces arrived per unit, zero between calls
   float* ws_o;      // [2P][Rcap][D] normalised partial outputs
   float* ws_lse;    // [2P][Rcap] partial log-sum-exp
@@ -162,16 +164,23 @@ struct Cfg {
 // Hand-offs between the waves of a workgroup go through LDS counters that
 // only grow: a wave adds one when it has done its part, and a waiting wave
 // polls until the counter reaches the total it needs.  The wait is bounded
-// (about 0.1 s of polling), so that a broken hand-off ends the kernel with
-// wrong results instead of hanging the GPU.
+// (about 0.1 s of polling by default), so that a broken hand-off ends the
+// kernel instead of hanging the GPU; a wait that gives up returns false, and
+// the kernel then raises the sticky give-up flag in the workspace.  With a
+// limit of 0 the counter is checked once.
 constexpr int kSpinLimit = 1 << 21;
-__device__ __forceinline__ void wait_count(int* c, int target) {
-  for (int spin = 0; spin < kSpinLimit; ++spin) {
-    if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) >= target)
-      break;
+constexpr int kGaveUp = 1;   // status-word bit: an in-kernel wait gave up
+__device__ __forceinline__ bool wait_count(int* c, int target, int limit) {
+  for (int spin = 0;; ++spin) {
+    if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) >= target) {
+      asm volatile("" ::: "memory");
+      return true;
+    }
+    if (spin >= limit) break;
     __builtin_amdgcn_s_sleep(1);
   }
   asm volatile("" ::: "memory");
+  return false;
 }
 // Count this wave once, after all of its earlier LDS operations (LDS serves
 // a wave's operations in order).
@@ -455,6 +464,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   __shared__ int full_cnt[kStages];       // producer waves whose loads of the stage's tile have landed
   __shared__ int empty_cnt[kStages];      // consumer waves done with the stage's tile
   __shared__ int cb_cnt;                  // consumer waves that reached a consumer barrier
+  __shared__ int pub_arrive[2];           // consumer waves whose stores of piece k have completed
 
   const int pid = blockIdx.x;
   const int tid = threadIdx.x;
@@ -466,6 +476,12 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   const int lm = lane & 15;               // row (or key, or d) inside a 16-wide MFMA block
   const int lg = lane >> 4;               // which quarter of the MFMA k dimension this lane feeds
   const int B = p.B, Hkv = p.Hkv, g = p.g;
+  // set when one of this wave's hand-off waits gave up; raised once in the
+  // workspace's sticky status word when the wave ends
+  bool gave_up = false;
+  auto report_give_up = [&](bool gave) {
+    if (gave && lane == 0) __hip_atomic_fetch_or(p.status, kGaveUp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  };
 
   // ---- padding rows c_b <= i < C_max of the sequences b = pid (mod P):
   // out = 0, lse = -inf; written by threads t0, t0 + stride, ...
@@ -561,6 +577,10 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       empty_cnt[lane] = 0;
     }
     if (lane == 0) cb_cnt = 0;
+    if (lane < 2) {
+      pub_arrive[lane] = 0;
+      sh_flag[lane] = 0;
+    }
     set_totals(total, ctotal);
     int g0 = 0, g1 = 0, nL = 0, s_last = 0;
     Cursor first = {0, 0, 0, 0u};
@@ -775,9 +795,10 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   };
 
   // Publication of pieces (at most two per workgroup: its first and last
-  // segment).  Two tiles after a piece's stores, the consumers wait for them
-  // (their own wait, which no tile load shares) and the piece is counted on
-  // its unit's arrival counter.  The counts are read back after the loop,
+  // segment).  Two tiles after a piece's stores, each consumer wave waits for
+  // its own stores (a wait no tile load shares) and arrives on an LDS
+  // counter; the last of the eight counts the piece on its unit's arrival
+  // counter.  The counts are read back after the loop,
   // where the last piece of a unit merges it.  The loop runs idle iterations
   // after the last tile until every piece is counted.
   struct Pub {
@@ -797,14 +818,17 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   float m_run = -INFINITY, l_lane = 0.f;
   Pub pub0 = {2, 0, 0}, pub1 = {2, 0, 0};
   int n_pub = 0;
-  // counter values before the two pieces (consumer thread 0), read after
-  // the loop, so the atomics' returns are never waited for inside it
-  int cnt0 = 0, cnt1 = 0;
+  // The consumer wave that counts piece k on its unit's arrival counter
+  // keeps the counter's previous value in cnt[k] (lane 0) and sets bit k of
+  // counted; both are read after the loop, so the atomic's return is never
+  // waited for inside it.
+  int cnt[2] = {0, 0};
+  int counted = 0;
   int ncb = 0;   // consumer barriers passed
   auto cbar = [&]() {
     ++ncb;
     signal_count(&cb_cnt);
-    wait_count(&cb_cnt, kConsumers * ncb);
+    gave_up |= !wait_count(&cb_cnt, kConsumers * ncb, p.spin_limit);
   };
 
   // The first unit's Q arrives through qn, so that qr is only ever written
@@ -828,8 +852,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     if constexpr (PAGED)
       if (v < count) pg = load_pages(cu);
     for (; v < count; v += 2) {
-      if (v >= 2) wait_count(&empty_cnt[grp], kConsumers * (v >> 1));
-      if (v == 1) wait_count(&full_cnt[0], 2);
+      if (v >= 2) gave_up |= !wait_count(&empty_cnt[grp], kConsumers * (v >> 1), p.spin_limit);
+      if (v == 1) gave_up |= !wait_count(&full_cnt[0], 2, p.spin_limit);
       dma(cu, grp, pg);
       if constexpr (PAGED) {
         // the next tile's table entries ride the wait for this tile's loads
@@ -848,6 +872,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         }
       }
     }
+    report_give_up(gave_up);
     return;
   }
   // Only the units of the range's first and last tile can be shared with
@@ -926,19 +951,28 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const bool due0 = pub0.state == 0 && v >= pub0.v + 2;
     const bool due1 = pub1.state == 0 && v >= pub1.v + 2;
     if (due0 || due1) {
+      // Every consumer wave stored its own rows and d blocks of the piece:
+      // each waits for its stores, then arrives on the piece's LDS counter,
+      // and the last wave to arrive counts the piece on the unit's arrival
+      // counter, after all eight waves' stores have completed.
+      const int k = due0 ? 0 : 1;
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's piece stores
-      Pub& q = due0 ? pub0 : pub1;
-      if (ctid == 0) {
-        const int old = __hip_atomic_fetch_add(p.counters + q.unit, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (due0) cnt0 = old;
-        else cnt1 = old;
+      int last = 0;
+      if (lane == 0)
+        last = __hip_atomic_fetch_add(&pub_arrive[k], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) ==
+               kConsumers - 1;
+      if (uniform(last)) {
+        if (lane == 0)
+          cnt[k] = __hip_atomic_fetch_add(p.counters + (k == 0 ? pub0 : pub1).unit, 1, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+        counted |= 1 << k;
       }
-      q.state = 1;
+      (k == 0 ? pub0 : pub1).state = 1;
     }
     if (v >= count) continue;
 
     const int st = v & 1;
-    wait_count(&full_cnt[st], 2 * ((v >> 1) + 1));   // tile v is in stage st
+    gave_up |= !wait_count(&full_cnt[st], 2 * ((v >> 1) + 1), p.spin_limit);   // tile v is in stage st
     const int b = cur.b, kvh = cur.kvh, j = cur.j;
     const uint32_t s = cur.s;
     const int n = seq_tiles<C>(s);
@@ -1220,18 +1254,17 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   }
 
   // ---- the last piece of a unit merges it, now that this workgroup's tiles
-  // are done
-  if (ctid == 0) {
+  // are done.  The wave that counted piece k sets its flag (sh_flag starts
+  // at 0: no merge here; else 1 + the entry of sh_share for the unit); that
+  // wave arrived last on the piece's LDS counter, after wave 0 had written
+  // sh_share.
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < 2; ++k) {
+    if ((counted >> k) & 1) {
       const Pub& q = k == 0 ? pub0 : pub1;
-      int flag = 0;   // 0: no merge here; else 1 + the entry of sh_share for the unit
-      if (q.state == 1) {
-        const int e = q.unit == sh_share[0][0] ? 0 : 1;
-        const int np = sh_share[e][2] - sh_share[e][1] + 1;   // pieces of the unit
-        flag = (k == 0 ? cnt0 : cnt1) + 1 == np ? 1 + e : 0;
-      }
-      sh_flag[k] = flag;
+      const int e = q.unit == sh_share[0][0] ? 0 : 1;
+      const int np = sh_share[e][2] - sh_share[e][1] + 1;   // pieces of the unit
+      if (lane == 0) sh_flag[k] = cnt[k] + 1 == np ? 1 + e : 0;
     }
   }
   cbar();
@@ -1239,6 +1272,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int f0 = sh_flag[0], f1 = sh_flag[1];
     if (f0 || f1) merge_units<D>(p, seqs, ctid, sh_share[f0 ? f0 - 1 : 0], sh_share[f1 ? f1 - 1 : 0], f0 != 0, f1 != 0);
   }
+  report_give_up(gave_up);
 }
 
 // Zero the per-unit counters of a workspace.
@@ -1258,12 +1292,14 @@ int key_tile(int dtype, int D) {
   return kHalf / (D * elt);
 }
 
-// Workspace layout: per-unit arrival counters for the largest launch (same
-// offsets for every descriptor with the same Hkv), then the partial results
-// of the pieces, two slots per workgroup.
+// Workspace layout: a 256-byte header holding the sticky status word, the
+// per-unit arrival counters for the largest launch (same offsets for every
+// descriptor with the same Hkv), then the partial results of the pieces, two
+// slots per workgroup.  The header and the counters form the zeroed region.
+constexpr size_t kHeaderBytes = 256;
 struct Plan {
   int g, P, Rcap;
-  size_t counter_bytes;
+  size_t zero_bytes;   // header + counters
   size_t slots, ws_lse_off, ws_o_off, ws_bytes;
 };
 
@@ -1276,7 +1312,7 @@ int validate_desc(const specmoe_verify_desc* d) {
   if (d->Hq % d->Hkv != 0) return SPECMOE_ERR_GQA;
   const int64_t g = d->Hq / d->Hkv;
   if ((int64_t)d->C_max * g > kMaxRows) return SPECMOE_ERR_ROWS;
-  if (d->flags != 0) return SPECMOE_ERR_FLAGS;
+  if ((d->flags & ~SPECMOE_FLAG_NO_WAIT) != 0) return SPECMOE_ERR_FLAGS;
   if (d->grid_blocks < 0 || d->grid_blocks > kMaxGrid) return SPECMOE_ERR_GRID;
   // partial results are addressed through 32-bit buffer descriptors
   const int64_t grid = d->grid_blocks ? d->grid_blocks : kDefaultGrid;
@@ -1303,19 +1339,18 @@ Plan make_plan(const specmoe_verify_desc* d) {
   pl.g = d->Hq / d->Hkv;
   pl.P = d->grid_blocks ? d->grid_blocks : kDefaultGrid;
   pl.Rcap = d->C_max * pl.g;
-  pl.counter_bytes = align256((size_t)kMaxSeqs * d->Hkv * sizeof(int));
+  pl.zero_bytes = kHeaderBytes + align256((size_t)kMaxSeqs * d->Hkv * sizeof(int));
   pl.slots = (size_t)2 * pl.P;
-  pl.ws_lse_off = pl.counter_bytes;
+  pl.ws_lse_off = pl.zero_bytes;
   pl.ws_o_off = pl.ws_lse_off + align256(pl.slots * pl.Rcap * sizeof(float));
   pl.ws_bytes = pl.ws_o_off + pl.slots * pl.Rcap * d->D * sizeof(float);
   return pl;
 }
 
 template <int ELT, int D, bool TREE, bool PAGED>
-void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_desc* d) {
+void launch(Params p, const Plan& pl, hipStream_t stream) {
   using C = Cfg<ELT != kF32, D>;
   const int B = p.B;
-  if (d->ev_main_begin) (void)hipEventRecord(static_cast<hipEvent_t>(d->ev_main_begin), stream);
   // batches beyond kMaxSeqs sequences run as consecutive launches on the stream
   for (int b0 = 0; b0 < B; b0 += kMaxSeqs) {
     Params s = p;
@@ -1335,34 +1370,31 @@ void launch(Params p, const Plan& pl, hipStream_t stream, const specmoe_verify_d
     s.lse = p.lse + (size_t)b0 * p.C_max * p.Hq;
     hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED>), dim3(pl.P), dim3(kThreads), 0, stream, s);
   }
-  if (d->ev_main_end) (void)hipEventRecord(static_cast<hipEvent_t>(d->ev_main_end), stream);
 }
 
 bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
 template <int ELT, bool PAGED>
-void launch_for_elt(int D, bool tree, const Params& p, const Plan& pl, hipStream_t s, const specmoe_verify_desc* d) {
+void launch_for_elt(int D, bool tree, const Params& p, const Plan& pl, hipStream_t s) {
   if (tree) {
-    if (D == 128) launch<ELT, 128, true, PAGED>(p, pl, s, d);
-    else launch<ELT, 64, true, PAGED>(p, pl, s, d);
+    if (D == 128) launch<ELT, 128, true, PAGED>(p, pl, s);
+    else launch<ELT, 64, true, PAGED>(p, pl, s);
   } else {
-    if (D == 128) launch<ELT, 128, false, PAGED>(p, pl, s, d);
-    else launch<ELT, 64, false, PAGED>(p, pl, s, d);
+    if (D == 128) launch<ELT, 128, false, PAGED>(p, pl, s);
+    else launch<ELT, 64, false, PAGED>(p, pl, s);
   }
 }
 
 template <bool PAGED>
-void launch_for_paging(int dtype, int D, bool tree, const Params& p, const Plan& pl, hipStream_t s,
-                       const specmoe_verify_desc* d) {
-  if (dtype == SPECMOE_BF16) launch_for_elt<kBF16, PAGED>(D, tree, p, pl, s, d);
-  else if (dtype == SPECMOE_F16) launch_for_elt<kF16, PAGED>(D, tree, p, pl, s, d);
-  else launch_for_elt<kF32, PAGED>(D, tree, p, pl, s, d);
+void launch_for_paging(int dtype, int D, bool tree, const Params& p, const Plan& pl, hipStream_t s) {
+  if (dtype == SPECMOE_BF16) launch_for_elt<kBF16, PAGED>(D, tree, p, pl, s);
+  else if (dtype == SPECMOE_F16) launch_for_elt<kF16, PAGED>(D, tree, p, pl, s);
+  else launch_for_elt<kF32, PAGED>(D, tree, p, pl, s);
 }
 
-void launch_for(int dtype, int D, bool tree, bool paged, const Params& p, const Plan& pl, hipStream_t s,
-                const specmoe_verify_desc* d) {
-  if (paged) launch_for_paging<true>(dtype, D, tree, p, pl, s, d);
-  else launch_for_paging<false>(dtype, D, tree, p, pl, s, d);
+void launch_for(int dtype, int D, bool tree, bool paged, const Params& p, const Plan& pl, hipStream_t s) {
+  if (paged) launch_for_paging<true>(dtype, D, tree, p, pl, s);
+  else launch_for_paging<false>(dtype, D, tree, p, pl, s);
 }
 
 // Host checks and launch of both entry points; draft_mask is NULL for a
@@ -1395,7 +1427,7 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   if (desc->B == 0) return SPECMOE_OK;   // nothing to read or write
   if (!q || !k_cache || !v_cache || !ctx_lens || !chunk_lens || !out || !lse) return SPECMOE_ERR_NULL_POINTER;
   if (tree && !draft_mask) return SPECMOE_ERR_NULL_POINTER;
-  if (!isfinite(scale)) return SPECMOE_ERR_SCALE;
+  if (!(scale > 0.f) || !isfinite(scale)) return SPECMOE_ERR_SCALE;
   if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(out)) return SPECMOE_ERR_ALIGN;
   if (tree && (reinterpret_cast<uintptr_t>(draft_mask) & 7u) != 0) return SPECMOE_ERR_ALIGN;
   if (is_paged && !block_table) return SPECMOE_ERR_NULL_POINTER;
@@ -1418,7 +1450,9 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
   p.pages_per_seq = is_paged ? paged->pages_per_seq : 0;
   p.num_pages = is_paged ? paged->num_pages : 0;
   char* ws = static_cast<char*>(desc->workspace);
-  p.counters = reinterpret_cast<int*>(ws);
+  p.status = reinterpret_cast<int*>(ws);
+  p.spin_limit = (desc->flags & SPECMOE_FLAG_NO_WAIT) ? 0 : kSpinLimit;
+  p.counters = reinterpret_cast<int*>(ws + kHeaderBytes);
   p.ws_lse = reinterpret_cast<float*>(ws + pl.ws_lse_off);
   p.ws_o = reinterpret_cast<float*>(ws + pl.ws_o_off);
   p.ws_lse_bytes = (int)(pl.ws_o_off - pl.ws_lse_off);
@@ -1435,7 +1469,7 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();  // clear a stale error from unrelated work
-  launch_for(desc->dtype, desc->D, tree, is_paged, p, pl, s, desc);
+  launch_for(desc->dtype, desc->D, tree, is_paged, p, pl, s);
   if (hipGetLastError() != hipSuccess) return SPECMOE_ERR_LAUNCH;
   return SPECMOE_OK;
 }
@@ -1457,11 +1491,24 @@ int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, 
   if (!aligned16(workspace)) return SPECMOE_ERR_ALIGN;
   const Plan pl = make_plan(desc);
   if (workspace_bytes < pl.ws_bytes) return SPECMOE_ERR_WORKSPACE;
-  const int n = (int)(pl.counter_bytes / sizeof(int));
+  const int n = (int)(pl.zero_bytes / sizeof(int));
   (void)hipGetLastError();
   hipLaunchKernelGGL(zero_counters_kernel, dim3((n + 255) / 256), dim3(256), 0, static_cast<hipStream_t>(stream),
                      static_cast<int*>(workspace), n);
   return hipGetLastError() == hipSuccess ? SPECMOE_OK : SPECMOE_ERR_LAUNCH;
+}
+
+int specmoe_verify_attn_status(const void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace) return SPECMOE_ERR_NULL_POINTER;
+  if (!aligned16(workspace)) return SPECMOE_ERR_ALIGN;
+  if (workspace_bytes < kHeaderBytes) return SPECMOE_ERR_WORKSPACE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int word = 0;
+  (void)hipGetLastError();
+  if (hipMemcpyAsync(&word, workspace, sizeof(word), hipMemcpyDeviceToHost, s) != hipSuccess)
+    return SPECMOE_ERR_LAUNCH;
+  if (hipStreamSynchronize(s) != hipSuccess) return SPECMOE_ERR_LAUNCH;
+  return (word & kGaveUp) ? SPECMOE_ERR_HANDOFF : SPECMOE_OK;
 }
 
 int32_t specmoe_verify_attn_key_tile(const specmoe_verify_desc* desc) {
@@ -1481,12 +1528,13 @@ const char* specmoe_status_str(int status) {
     case SPECMOE_ERR_DTYPE: return "unsupported dtype";
     case SPECMOE_ERR_ROWS: return "C_max * (Hq / Hkv) exceeds 128 query rows per KV head";
     case SPECMOE_ERR_GRID: return "grid_blocks must be 0 (default) or in [1, 2048], with partial results under 2 GB";
-    case SPECMOE_ERR_FLAGS: return "flags is reserved and must be 0";
+    case SPECMOE_ERR_FLAGS: return "flags may only hold SPECMOE_FLAG_NO_WAIT";
     case SPECMOE_ERR_WORKSPACE: return "workspace too small";
     case SPECMOE_ERR_ALIGN: return "q, k_cache, v_cache, out and workspace must be 16-byte aligned";
-    case SPECMOE_ERR_SCALE: return "scale is not finite";
+    case SPECMOE_ERR_SCALE: return "scale must be finite and positive";
     case SPECMOE_ERR_LAUNCH: return "HIP kernel launch failed";
     case SPECMOE_ERR_MASK: return "draft masks hold at most 64 draft tokens: C_max must be <= 64";
+    case SPECMOE_ERR_HANDOFF: return "an in-kernel wait for another wave gave up: results of a call are unspecified";
     case SPECMOE_ERR_PAGES:
       return "page_size must be a power of two in [8, 65536], pages_per_seq and num_pages positive, "
              "S_max = page_size * pages_per_seq";

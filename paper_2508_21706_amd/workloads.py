@@ -222,7 +222,7 @@ def kv_slab(w: Workload, b: int, T_b: int, which: str) -> np.ndarray:
 
 def make_inputs(w: Workload, fill: float = float("nan"),
                 batches: Optional[Sequence[int]] = None,
-                ctx_lens=None, chunk_lens=None):
+                ctx_lens=None, chunk_lens=None, workers: int = 0):
     """Materialise workload ``w`` on the host.
 
     Returns a dict with q [B, C_max, Hq, D], k_cache / v_cache
@@ -231,6 +231,8 @@ def make_inputs(w: Workload, fill: float = float("nan"),
     [B, C_max] words of a tree workload, else None).  ``batches`` restricts the
     cache fill to those sequences (others keep ``fill``), for sampled checks of
     large workloads.  ``ctx_lens`` / ``chunk_lens`` override the drawn lengths.
+    ``workers`` > 1 draws the sequences' slabs in that many threads (each
+    slab has its own generator, so the values do not depend on it).
     """
     ctx, chunk = draw_lengths(w)
     if ctx_lens is not None:
@@ -249,10 +251,19 @@ def make_inputs(w: Workload, fill: float = float("nan"),
     k = np.full((B, w.Hkv, S, w.D), fv, dtype=store)
     v = np.full((B, w.Hkv, S, w.D), fv, dtype=store)
     todo = range(B) if batches is None else batches
-    for b in todo:
+
+    def fill_seq(b):
         T_b = int(ctx[b]) + int(chunk[b])
         k[b, :, :T_b] = kv_slab(w, b, T_b, "k")
         v[b, :, :T_b] = kv_slab(w, b, T_b, "v")
+
+    if workers > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(workers) as ex:
+            list(ex.map(fill_seq, todo))
+    else:
+        for b in todo:
+            fill_seq(b)
     draft_mask = tree_draft_masks(w.index, chunk, w.C_max) if w.draft == "tree" else None
     out = dict(q=q, k_cache=k, v_cache=v, ctx_lens=ctx, chunk_lens=chunk,
                scale=w.scale, workload=w, draft_mask=draft_mask)

@@ -70,8 +70,8 @@ def _call(lib, desc, q=FAKE, k=FAKE, v=FAKE, ctx=FAKE, chunk=FAKE, scale=0.088, 
     (dict(C_max=17, Hq=32, Hkv=4), -6),          # 17 * 8 = 136 rows > 128
     (dict(grid_blocks=-1), -7),
     (dict(grid_blocks=2049), -7),
-    (dict(flags=1), -12),
-    (dict(flags=2), -12),
+    (dict(flags=2), -12),                        # only SPECMOE_FLAG_NO_WAIT is defined
+    (dict(flags=3), -12),
     (dict(S_max=1 << 23), -2),                   # slab offsets would pass 2^31 bytes
     (dict(S_max=1 << 24, dtype=bd.SPECMOE_BF16, D=64), -2),   # packed lengths need T < 2^24
 ])
@@ -90,6 +90,21 @@ def test_null_and_alignment_and_scale(lib):
         assert _call(lib, d, **{arg: FAKE + 4}) == -9, arg
     assert _call(lib, d, scale=float("nan")) == -10
     assert _call(lib, d, scale=float("inf")) == -10
+    # the kernels track the running maximum of scale * q.k as scale times the
+    # maximum of q.k, which needs scale > 0
+    for bad in (0.0, -0.0, -0.088, -float("inf")):
+        assert _call(lib, d, scale=bad) == -10, bad
+    assert _call(lib, d, scale=1e-30) != -10
+
+
+def test_descriptor_struct_matches_header():
+    """The binding's mirror of specmoe_verify_desc has the header's fields, in
+    order (no timing or other hidden fields)."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct specmoe_verify_desc \{(.*?)\} specmoe_verify_desc;", text, re.S).group(1)
+    fields = re.findall(r"(\w+)\s*;", body)
+    assert fields == [f[0] for f in bd.Desc._fields_]
+    assert ctypes.sizeof(bd.Desc) == 56
 
 
 def _call_tree(lib, desc, mask=FAKE, **kw):
@@ -134,8 +149,9 @@ def test_workspace_contract(lib):
     rows = 5 * 4                                # C_max * g
     slots = 2 * 256 * rows                      # two pieces per workgroup
     counters = 1024 * 8 * 4                     # one per (sequence, KV head) of a launch
-    assert need >= counters + slots * (128 + 1) * 4
-    assert need < counters + slots * (128 + 1) * 4 + 512
+    header = 256                                # the sticky status word
+    assert need >= header + counters + slots * (128 + 1) * 4
+    assert need < header + counters + slots * (128 + 1) * 4 + 512
     # the workspace grows with the grid
     d2 = _desc(B=64, grid_blocks=1024)
     assert lib.specmoe_verify_attn_workspace_bytes(ctypes.byref(d2)) > need
@@ -152,6 +168,11 @@ def test_workspace_contract(lib):
     assert init(FAKE, need - 1, None, ctypes.byref(_desc(B=64))) == -8
     assert init(FAKE + 4, need, None, ctypes.byref(_desc(B=64))) == -9
     assert init(FAKE, need, None, ctypes.byref(_desc(B=64, D=80))) == -4
+    # the status query validates before its copy
+    status = lib.specmoe_verify_attn_status
+    assert status(None, need, None) == -1
+    assert status(FAKE + 4, need, None) == -9
+    assert status(FAKE, 255, None) == -8
 
 
 def test_key_tile(lib):

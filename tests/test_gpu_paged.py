@@ -44,42 +44,6 @@ def test_paged_workload_reduced_batch():
             check_paged(inp, w.dtype, ps, f"{w.name}[B=6]", grid_blocks=P)
 
 
-def test_paged_workload_full_size_sampled():
-    """The full paged workload (16-token pages in a shuffled pool) in the
-    benchmark's launch configuration; the oracle checks sampled sequences."""
-    w = wl.get("mixtral_paged_b64")
-    ctx, chunk = wl.draw_lengths(w)
-    rng = np.random.default_rng(79)
-    sample = sorted({0, w.B - 1, int(np.argmin(ctx)), int(np.argmax(ctx)),
-                     *rng.choice(w.B, 2, replace=False).tolist()})
-    note(f"case {w.name} full size, sampled sequences {sample}")
-    host = wl.make_inputs(w, batches=sample)
-    # the unsampled sequences' pages hold finite values
-    d = dev()
-    kp = to_dev(host["k_pages"], "bf16")
-    vp = to_dev(host["v_pages"], "bf16")
-    table = host["block_table"]
-    g = torch.Generator(device=d)
-    g.manual_seed(2000)
-    others = np.setdiff1d(np.arange(w.B), sample)
-    fill = torch.from_numpy(table[others].ravel().astype(np.int64)).to(d)
-    kp[fill] = torch.randn((len(fill),) + tuple(kp.shape[1:]), generator=g, device=d).to(torch.bfloat16)
-    vp[fill] = torch.randn((len(fill),) + tuple(vp.shape[1:]), generator=g, device=d).to(torch.bfloat16)
-    out, lse = nan_outputs(w.B, w.C_max, w.Hq, w.D)
-    pkg.verify_attn_paged(to_dev(host["q"], "bf16"), kp, vp, i32(table), i32(ctx), i32(chunk), w.scale,
-                          out=out, lse=lse)
-    torch.cuda.synchronize()
-    units = [(b, h) for b in sample for h in range(w.Hkv)]
-    ref_o, ref_l = verify_attn_ref(host["q"], host["k_cache"], host["v_cache"], ctx, chunk, w.scale, w.dtype,
-                                   units=units)
-    o = out.cpu().double().numpy()
-    s = lse.cpu().double().numpy()
-    compare(o, s, ref_o, ref_l, w.dtype, f"{w.name} full-size sampled")
-    rows = np.arange(w.C_max)[None, :] < chunk[:, None]
-    assert np.all(np.isfinite(o[rows])) and np.all(np.isfinite(s[rows]))
-    assert np.all(o[~rows] == 0.0) and np.all(s[~rows] == -np.inf)
-
-
 PAGED_EDGE = {
     # name: (B, Hq, Hkv, D, dtype, ctx, chunk, C_max, page sizes)
     "bf16_d64_256_key_tiles": (3, 16, 4, 64, "bf16", [500, 260, 1], [5, 3, 5], 5, (8, 32, 256)),

@@ -6,6 +6,7 @@ Tolerances (written here, applied to every valid row):
 Padding rows (i >= c_b) must be exactly out = 0, lse = -inf.  Unused cache
 rows and query rows are NaN-poisoned, so any read of them shows up as NaN.
 """
+import ctypes
 import dataclasses
 import sys
 
@@ -104,56 +105,6 @@ def test_workload_reduced_batch(name):
     inp = wl.make_inputs(w)
     for P in (0, 1, 5, 64, 300, 2048):
         check_case(inp, w.dtype, f"{name}[B={nb}]", grid_blocks=P)
-
-
-def _full_size_inputs(w, sample):
-    """Full-size workload on the GPU: every sequence holds N(0,1) values of the
-    workload's 16-bit type from torch's generator except the sampled ones,
-    which hold the recipe's values (NaN-poisoned outside their valid rows) and
-    are checked by the oracle."""
-    ctx, chunk = wl.draw_lengths(w)
-    d = dev()
-    g = torch.Generator(device=d)
-    g.manual_seed(1000 + w.index)
-    shape = (w.B, w.Hkv, w.S_max, w.D)
-    k = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(TORCH16[w.dtype])
-    v = torch.randn(shape, generator=g, device=d, dtype=torch.float32).to(TORCH16[w.dtype])
-    host = wl.make_inputs(w, batches=sample)
-    for b in sample:
-        k[b] = to_dev(host["k_cache"][b], w.dtype)
-        v[b] = to_dev(host["v_cache"][b], w.dtype)
-    return host, to_dev(host["q"], w.dtype), k, v, ctx, chunk
-
-
-@pytest.mark.parametrize("name", ["mixtral_b64", "large_batch_b256", "long_ctx_b32", "ragged_chunk_b128",
-                                  "eagle_draft_b64", "mixtral_f16_b64"])
-def test_workload_full_size_sampled(name):
-    """Full-size workload in the benchmark's launch configuration (default
-    grid); the oracle checks sampled sequences, every output row is
-    checked for finiteness and padding."""
-    w = wl.get(name)
-    ctx, chunk = wl.draw_lengths(w)
-    rng = np.random.default_rng(77)
-    sample = sorted({0, w.B - 1, int(np.argmin(ctx)), int(np.argmax(ctx)),
-                     *rng.choice(w.B, 2, replace=False).tolist()})
-    note(f"case {name} full size, sampled sequences {sample}")
-    host, q, k, v, ctx, chunk = _full_size_inputs(w, sample)
-    d = dev()
-    out, lse = nan_outputs(w.B, w.C_max, w.Hq, w.D)
-    pkg.verify_attn(q, k, v, torch.from_numpy(ctx).to(d), torch.from_numpy(chunk).to(d), w.scale, out=out, lse=lse)
-    torch.cuda.synchronize()
-    units = [(b, h) for b in sample for h in range(w.Hkv)]
-    ref_o, ref_l = verify_attn_ref(host["q"], host["k_cache"], host["v_cache"], ctx, chunk, w.scale,
-                                   w.dtype, units=units)
-    o = out.cpu().double().numpy()
-    s = lse.cpu().double().numpy()
-    compare(o, s, ref_o, ref_l, w.dtype, f"{name} full-size sampled")
-    # every row of the whole batch: finite where valid, exact padding elsewhere
-    rows = np.arange(w.C_max)[None, :] < chunk[:, None]
-    assert np.all(np.isfinite(o[rows])) and np.all(np.isfinite(s[rows]))
-    assert np.all(o[~rows] == 0.0) and np.all(s[~rows] == -np.inf)
-    del k, v, q, out, lse
-    torch.cuda.empty_cache()
 
 
 # ------------------------------------------------------------- edge cases
@@ -301,3 +252,64 @@ def test_workspace_reuse_across_calls():
     # the per-unit counters at the start of the workspace are back to zero
     counters = ws[: 1024 * w.Hkv * 4].view(torch.int32).cpu()
     assert int(counters.abs().sum()) == 0
+
+
+def test_handoff_give_up_is_reported():
+    """A call whose in-kernel waits are told to give up at once (the
+    diagnostic flag; every kernel still ends normally and stays in bounds)
+    leaves the sticky give-up bit in its workspace; the status query reports
+    it until the workspace is initialised again, after which a normal call is
+    correct and reports nothing."""
+    d = dev()
+    w = dataclasses.replace(wl.get("mixtral_b64"), B=8)
+    inp = wl.make_inputs(w)
+    args = (to_dev(inp["q"], "bf16"), to_dev(inp["k_cache"], "bf16"), to_dev(inp["v_cache"], "bf16"),
+            torch.from_numpy(inp["ctx_lens"]).to(d), torch.from_numpy(inp["chunk_lens"]).to(d), w.scale)
+    desc = pkg.desc_for(args[0], args[1], grid_blocks=16)
+    ws = pkg.alloc_workspace(desc, d)
+    assert pkg.workspace_status(ws) == 0
+    note("case give-up forced from the host (flags = SPECMOE_FLAG_NO_WAIT), grid 16")
+    pkg.verify_attn(*args, workspace=ws, grid_blocks=16, flags=pkg.binding.SPECMOE_FLAG_NO_WAIT)
+    torch.cuda.synchronize()
+    assert pkg.workspace_status(ws) == -15
+    assert pkg.workspace_status(ws) == -15          # sticky
+    # a give-up may also leave arrival counters set (a merge whose barrier
+    # gave up is skipped): re-initialising clears the status word and them
+    st = pkg.load_library().specmoe_verify_attn_workspace_init(
+        ws.data_ptr(), ws.numel(), torch.cuda.current_stream(d).cuda_stream, ctypes.byref(desc))
+    assert st == 0
+    assert pkg.workspace_status(ws) == 0
+    counters = ws[256: 256 + 1024 * w.Hkv * 4].view(torch.int32).cpu()
+    assert int(counters.abs().sum()) == 0
+    out, lse = nan_outputs(w.B, w.C_max, w.Hq, w.D)
+    pkg.verify_attn(*args, out=out, lse=lse, workspace=ws, grid_blocks=16)
+    torch.cuda.synchronize()
+    assert pkg.workspace_status(ws) == 0
+    ref_o, ref_l = verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], inp["ctx_lens"], inp["chunk_lens"],
+                                   w.scale, "bf16")
+    compare(out.cpu().double().numpy(), lse.cpu().double().numpy(), ref_o, ref_l, "bf16", "after a give-up")
+
+
+def test_side_stream_without_workspace():
+    """A call on a non-current stream without a workspace: the binding takes
+    the workspace (and outputs) from that stream's pool, so allocations on
+    the current stream right after the call cannot reuse the workspace while
+    the kernel still runs."""
+    d = dev()
+    w = dataclasses.replace(wl.get("ragged_chunk_b128"), B=24)
+    inp = wl.make_inputs(w)
+    args = (to_dev(inp["q"], "bf16"), to_dev(inp["k_cache"], "bf16"), to_dev(inp["v_cache"], "bf16"),
+            torch.from_numpy(inp["ctx_lens"]).to(d), torch.from_numpy(inp["chunk_lens"]).to(d), w.scale)
+    ref_o, ref_l = verify_attn_ref(inp["q"], inp["k_cache"], inp["v_cache"], inp["ctx_lens"], inp["chunk_lens"],
+                                   w.scale, "bf16")
+    side = torch.cuda.Stream(device=d)
+    side.wait_stream(torch.cuda.current_stream(d))
+    for trial in range(3):
+        note(f"case side stream, no workspace, trial {trial}")
+        out, lse = pkg.verify_attn(*args, grid_blocks=64, stream=side)
+        # the current stream allocates and fills buffers meanwhile
+        junk = [torch.full((1 << 20,), 7, dtype=torch.int32, device=d) for _ in range(8)]
+        del junk
+        torch.cuda.synchronize()
+        compare(out.cpu().double().numpy(), lse.cpu().double().numpy(), ref_o, ref_l, "bf16",
+                f"side stream {trial}")
