@@ -1,4 +1,6 @@
-"""Build step: compile the HIP kernels and C-ABI into libspecmoe_verify.so.
+"""Build step: compile the HIP kernels and C-ABI into libspecmoe_verify.so,
+and the benchmark's streaming-read probe into its own libspecmoe_probe.so
+(not part of the library).
 
 Cross-compiles for gfx950 (MI355X) with hipcc; no GPU is needed to build.
 Packed-FP32 instructions are disabled for all device code.
@@ -15,6 +17,8 @@ ROOT = os.path.dirname(HERE)
 SOURCES = [os.path.join(HERE, "csrc", "verify_attn.hip"), os.path.join(HERE, "csrc", "accept.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 OUTPUT = os.path.join(HERE, "libspecmoe_verify.so")
+PROBE_SOURCES = [os.path.join(HERE, "csrc", "stream_probe.hip")]
+PROBE_OUTPUT = os.path.join(HERE, "libspecmoe_probe.so")
 ARCH = "gfx950"
 
 
@@ -25,16 +29,23 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build_command(output: str = OUTPUT, extra=()):
+def build_command(output: str = OUTPUT, extra=(), sources=SOURCES):
     return [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            f"-I{INCLUDE}", *extra, *SOURCES, "-o", output]
+            f"-I{INCLUDE}", *extra, *sources, "-o", output]
 
 
 def build(verbose: bool = False, output: str = OUTPUT) -> str:
-    """Compile the library (always, even if a build is present); return its path."""
+    """Compile the library and the probe (always, even if builds are present);
+    return the library's path."""
+    _compile(SOURCES, output, verbose)
+    _compile(PROBE_SOURCES, PROBE_OUTPUT, verbose)
+    return output
+
+
+def _compile(sources, output: str, verbose: bool) -> None:
     tmp = output + ".tmp"
-    cmd = build_command(tmp)
+    cmd = build_command(tmp, sources=sources)
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -51,7 +62,6 @@ def build(verbose: bool = False, output: str = OUTPUT) -> str:
     if check.returncode != 0:
         raise RuntimeError(f"built library does not load:\n{check.stderr.strip().splitlines()[-1]}")
     os.replace(tmp, output)
-    return output
 
 
 if __name__ == "__main__":
