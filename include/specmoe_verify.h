@@ -191,6 +191,37 @@ int specmoe_verify_attn_tree(const void* q, const void* k_cache, const void* v_c
                              const uint64_t* draft_mask, float scale, float* out, float* lse,
                              void* stream, const specmoe_verify_desc* desc);
 
+/*
+ * specmoe_verify_attn_noalloc -- specmoe_verify_attn for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * and harnesses that forbid hipMalloc.
+ *
+ * The same operation, arguments, layouts, preconditions, determinism and
+ * errors as specmoe_verify_attn, except that desc->workspace and
+ * desc->workspace_bytes are ignored: the kernels use a scratch array that
+ * the library holds in static device memory, one per GPU (48 MiB, held until
+ * the process ends), instead of a caller workspace.  Before the first call on
+ * a device, its address is looked up once with that device current.  No call
+ * allocates or frees anything (no hipMalloc, hipFree or allocating library
+ * routine); each enqueues a small kernel that clears the scratch's arrival
+ * counters, then the attention kernel, on `stream`.
+ *
+ * Limit: the workspace the descriptor needs
+ * (specmoe_verify_attn_workspace_bytes) must fit in 48 MiB, which holds
+ * every shape at the default grid; a larger need returns
+ * SPECMOE_ERR_WORKSPACE before any HIP call.
+ *
+ * Every call on one GPU shares that GPU's scratch: calls that may overlap on
+ * one GPU (on different streams, or from several host threads without
+ * ordering) race and give unspecified results; serialise them, e.g. on one
+ * stream.  A give-up of an in-kernel wait is recorded in the scratch's
+ * status word, which specmoe_verify_attn_status(NULL, 0, stream) reads.
+ */
+int specmoe_verify_attn_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                                const int32_t* ctx_lens, const int32_t* chunk_lens,
+                                float scale, float* out, float* lse, void* stream,
+                                const specmoe_verify_desc* desc);
+
 /* Geometry of a paged KV cache (host struct). */
 typedef struct specmoe_paged_kv {
   int32_t page_size;      /* tokens per page: a power of two in [8, 65536]            */
@@ -260,7 +291,10 @@ int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, 
  * it reports every call enqueued on it before; the word stays set until
  * specmoe_verify_attn_workspace_init clears it.  After SPECMOE_ERR_HANDOFF
  * the workspace must be initialised again before its next call: a give-up
- * can also leave arrival counters set.  SPECMOE_ERR_NULL_POINTER,
+ * can also leave arrival counters set.  workspace = NULL with
+ * workspace_bytes = 0 reads the status word of the current device's static
+ * scratch (specmoe_verify_attn_noalloc), which stays set until the process
+ * ends.  SPECMOE_ERR_NULL_POINTER,
  * SPECMOE_ERR_ALIGN, SPECMOE_ERR_WORKSPACE (fewer than 256 bytes) or
  * SPECMOE_ERR_LAUNCH (HIP reported an error for the copy) otherwise. */
 int specmoe_verify_attn_status(const void* workspace, size_t workspace_bytes, void* stream);

@@ -9,6 +9,7 @@ synthetic inputs.
 from .binding import (AcceptDesc, Desc, SpecMoEError, accept_desc, accept_greedy, accept_greedy_tree,  # noqa: F401
                       compact_accepted_kv,
                       alloc_accept_workspace, alloc_workspace, desc_for, key_tile, load_library, make_desc,
-                      status_str, verify_attn, verify_attn_paged, verify_attn_tree, workspace_bytes,
+                      status_str, verify_attn, verify_attn_noalloc, verify_attn_paged, verify_attn_tree,
+                      workspace_bytes,
                       workspace_status)
 from . import binding  # noqa: F401

@@ -76,6 +76,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.specmoe_verify_attn.argtypes = [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
         ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(Desc)]
+    lib.specmoe_verify_attn_noalloc.restype = ctypes.c_int
+    lib.specmoe_verify_attn_noalloc.argtypes = lib.specmoe_verify_attn.argtypes
     lib.specmoe_verify_attn_tree.restype = ctypes.c_int
     lib.specmoe_verify_attn_tree.argtypes = [
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
@@ -164,13 +166,18 @@ def alloc_workspace(desc: Desc, device, stream: Optional[torch.cuda.Stream] = No
     return ws
 
 
-def workspace_status(workspace: torch.Tensor, stream: Optional[torch.cuda.Stream] = None) -> int:
+def workspace_status(workspace: Optional[torch.Tensor], stream: Optional[torch.cuda.Stream] = None) -> int:
     """``specmoe_verify_attn_status``: synchronises with the stream and returns
     0 (SPECMOE_OK) or -15 (SPECMOE_ERR_HANDOFF: an in-kernel wait gave up in a
-    call since the workspace was initialised)."""
-    s = stream if stream is not None else torch.cuda.current_stream(workspace.device)
-    st = load_library().specmoe_verify_attn_status(workspace.data_ptr(),
-                                                    workspace.numel() * workspace.element_size(), s.cuda_stream)
+    call since the workspace was initialised).  ``workspace=None``: the
+    current device's static scratch of ``verify_attn_noalloc``."""
+    if workspace is None:
+        s = stream if stream is not None else torch.cuda.current_stream()
+        st = load_library().specmoe_verify_attn_status(None, 0, s.cuda_stream)
+    else:
+        s = stream if stream is not None else torch.cuda.current_stream(workspace.device)
+        st = load_library().specmoe_verify_attn_status(workspace.data_ptr(),
+                                                        workspace.numel() * workspace.element_size(), s.cuda_stream)
     if st not in (0, -15):
         raise SpecMoEError(st, status_str(st))
     return st
@@ -206,6 +213,37 @@ def verify_attn(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
     """
     return _call(q, k_cache, v_cache, ctx_lens, chunk_lens, None, scale, out, lse, workspace, grid_blocks,
                  stream, flags, check_lengths)
+
+
+def verify_attn_noalloc(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                        ctx_lens: torch.Tensor, chunk_lens: torch.Tensor, scale: float,
+                        out: torch.Tensor, lse: torch.Tensor, grid_blocks: int = 0,
+                        stream: Optional[torch.cuda.Stream] = None):
+    """``specmoe_verify_attn_noalloc``: chain drafts like ``verify_attn``,
+    with the library's static per-GPU scratch instead of a workspace.  The
+    caller passes ``out`` and ``lse``; nothing is allocated.  Calls that may
+    overlap on one GPU race (they share the scratch)."""
+    lib = load_library()
+    B, C_max, Hq, D = q.shape
+    if k_cache.dim() != 4:
+        raise ValueError("k_cache must be [B, Hkv, S_max, D]")
+    _, Hkv, S_max, _ = k_cache.shape
+    dt = q.dtype
+    _check(q, "q", (B, C_max, Hq, D), dt)
+    _check(k_cache, "k_cache", (B, Hkv, S_max, D), dt)
+    _check(v_cache, "v_cache", (B, Hkv, S_max, D), dt)
+    _check(ctx_lens, "ctx_lens", (B,), torch.int32)
+    _check(chunk_lens, "chunk_lens", (B,), torch.int32)
+    _check(out, "out", (B, C_max, Hq, D), torch.float32)
+    _check(lse, "lse", (B, C_max, Hq), torch.float32)
+    desc = make_desc(B, Hq, Hkv, D, C_max, S_max, _dtype_code(q), grid_blocks)
+    s = stream if stream is not None else torch.cuda.current_stream(q.device)
+    st = lib.specmoe_verify_attn_noalloc(q.data_ptr(), k_cache.data_ptr(), v_cache.data_ptr(), ctx_lens.data_ptr(),
+                                         chunk_lens.data_ptr(), float(scale), out.data_ptr(), lse.data_ptr(),
+                                         s.cuda_stream, ctypes.byref(desc))
+    if st != 0:
+        raise SpecMoEError(st, status_str(st))
+    return out, lse
 
 
 def verify_attn_tree(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,

@@ -58,9 +58,19 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "specmoe_verify.h"
+
+// Device scratch of specmoe_verify_attn_noalloc (for callers that cannot
+// allocate): the workspace layout of a normal call (header, arrival
+// counters, partial results) in one file-scope array per GPU, held until the
+// process ends.  Host code never passes the array's name to a kernel (on the
+// host it is only a stand-in for the symbol): it uses the device address
+// that hipGetSymbolAddress returns for the current device.
+constexpr size_t kScratchBytes = (size_t)48 << 20;
+static __device__ __attribute__((aligned(256))) char scratch[kScratchBytes];
 
 namespace {
 
@@ -1179,11 +1189,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
       const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
       if (nks > 1) {
-        char* scratch = smem + st * C::kStage;
+        char* merge_lds = smem + st * C::kStage;
         cbar();   // every consumer is done with this tile's stage
         if (active) {
           const int region = rb * nks + kslot;
-          f32x4* reg = reinterpret_cast<f32x4*>(scratch + region * (64 * D));
+          f32x4* reg = reinterpret_cast<f32x4*>(merge_lds + region * (64 * D));
           // the d blocks the other waves of the row block merge (this wave
           // keeps its own slice in registers)
 #pragma unroll
@@ -1218,7 +1228,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 #pragma unroll
               for (int k = 0; k < kConsumers; ++k) {
                 if (k < nks) {
-                  const f32x4* reg = reinterpret_cast<const f32x4*>(scratch + (rb * nks + k) * (64 * D));
+                  const f32x4* reg = reinterpret_cast<const f32x4*>(merge_lds + (rb * nks + k) * (64 * D));
                   acc += (k == kslot ? o[db] : reg[db * 64 + lane]) * wk[k];
                 }
               }
@@ -1415,7 +1425,7 @@ int validate_pages(const specmoe_verify_desc* d, const specmoe_paged_kv* pk) {
 int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* ctx_lens,
         const int32_t* chunk_lens, const uint64_t* draft_mask, bool tree, float scale, float* out, float* lse,
         void* stream, const specmoe_verify_desc* desc, const int32_t* block_table = nullptr,
-        const specmoe_paged_kv* paged = nullptr) {
+        const specmoe_paged_kv* paged = nullptr, bool clear_counters = false) {
   const int st = validate_desc(desc);
   if (st != SPECMOE_OK) return st;
   if (tree && desc->C_max > kMaxDraftBits) return SPECMOE_ERR_MASK;
@@ -1469,8 +1479,33 @@ int run(const void* q, const void* k_cache, const void* v_cache, const int32_t* 
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();  // clear a stale error from unrelated work
+  if (clear_counters) {
+    // the arrival counters of the units of one launch (at most kMaxSeqs
+    // sequences), zeroed by a small kernel ahead of the main one
+    const int n = (desc->B < kMaxSeqs ? desc->B : kMaxSeqs) * desc->Hkv;
+    hipLaunchKernelGGL(zero_counters_kernel, dim3((n + 255) / 256), dim3(256), 0, s, p.counters, n);
+  }
   launch_for(desc->dtype, desc->D, tree, is_paged, p, pl, s);
   if (hipGetLastError() != hipSuccess) return SPECMOE_ERR_LAUNCH;
+  return SPECMOE_OK;
+}
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_for_current_device(void** ptr_out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return SPECMOE_ERR_LAUNCH;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return SPECMOE_ERR_LAUNCH;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *ptr_out = g_scratch_ptr[dev];
   return SPECMOE_OK;
 }
 
@@ -1499,6 +1534,13 @@ int specmoe_verify_attn_workspace_init(void* workspace, size_t workspace_bytes, 
 }
 
 int specmoe_verify_attn_status(const void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace && workspace_bytes == 0) {   // the current device's static scratch
+    void* ptr = nullptr;
+    const int st = scratch_for_current_device(&ptr);
+    if (st != SPECMOE_OK) return st;
+    workspace = ptr;
+    workspace_bytes = kScratchBytes;
+  }
   if (!workspace) return SPECMOE_ERR_NULL_POINTER;
   if (!aligned16(workspace)) return SPECMOE_ERR_ALIGN;
   if (workspace_bytes < kHeaderBytes) return SPECMOE_ERR_WORKSPACE;
@@ -1546,6 +1588,23 @@ int specmoe_verify_attn(const void* q, const void* k_cache, const void* v_cache,
                         const int32_t* chunk_lens, float scale, float* out, float* lse, void* stream,
                         const specmoe_verify_desc* desc) {
   return run(q, k_cache, v_cache, ctx_lens, chunk_lens, nullptr, false, scale, out, lse, stream, desc);
+}
+
+int specmoe_verify_attn_noalloc(const void* q, const void* k_cache, const void* v_cache, const int32_t* ctx_lens,
+                                const int32_t* chunk_lens, float scale, float* out, float* lse, void* stream,
+                                const specmoe_verify_desc* desc) {
+  const int st = validate_desc(desc);
+  if (st != SPECMOE_OK) return st;
+  if (make_plan(desc).ws_bytes > kScratchBytes) return SPECMOE_ERR_WORKSPACE;
+  if (desc->B == 0) return SPECMOE_OK;
+  void* ws = nullptr;
+  const int ss = scratch_for_current_device(&ws);
+  if (ss != SPECMOE_OK) return ss;
+  specmoe_verify_desc d = *desc;
+  d.workspace = ws;
+  d.workspace_bytes = kScratchBytes;
+  return run(q, k_cache, v_cache, ctx_lens, chunk_lens, nullptr, false, scale, out, lse, stream, &d, nullptr, nullptr,
+             true);
 }
 
 int specmoe_verify_attn_tree(const void* q, const void* k_cache, const void* v_cache, const int32_t* ctx_lens,

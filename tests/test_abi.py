@@ -185,6 +185,21 @@ def test_key_tile(lib):
     assert lib.specmoe_verify_attn_key_tile(ctypes.byref(_desc(dtype=3))) == -5
 
 
+def test_noalloc_host_checks(lib):
+    """The allocation-free entry point validates like the others and refuses
+    a problem whose workspace would not fit its static scratch, before any
+    HIP call."""
+    call = lib.specmoe_verify_attn_noalloc
+    args = (FAKE, FAKE, FAKE, FAKE, FAKE, 0.088, FAKE, FAKE, None)
+    assert call(*args, None) == -1
+    assert call(*args, ctypes.byref(_desc(D=96))) == -4
+    assert call(*args, ctypes.byref(_desc(flags=2))) == -12
+    # 2 * 2048 workgroups * 128 rows * (128 + 1) * 4 bytes > 48 MiB of scratch
+    assert call(*args, ctypes.byref(_desc(C_max=16, Hq=32, Hkv=4, grid_blocks=2048))) == -8
+    assert call(None, None, None, None, None, 0.088, None, None, None, ctypes.byref(_desc(B=0))) == 0
+    assert call(*args[:5], -1.0, *args[6:], ctypes.byref(_desc(B=0))) == 0   # B = 0: nothing is looked at
+
+
 def test_empty_batch_is_a_no_op(lib):
     # B = 0 returns before any HIP call and before looking at data pointers
     assert _call(lib, _desc(B=0)) == 0
