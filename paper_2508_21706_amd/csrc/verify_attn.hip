@@ -166,7 +166,13 @@ struct Cfg {
   static constexpr int kDB = D / 16;                        // 16-wide d blocks of O^T
   static constexpr int kQJ = kChunks / 4;                   // 16-byte Q chunks per lane
   static_assert(kInstK <= 2 * kMaxDma && kInstV <= 2 * kMaxDma, "DMA instructions per producer wave");
-  static_assert(kStages * kStage + 12 * 1024 + 256 <= 160 * 1024, "LDS budget");
+  // LDS beside the stages: packed lengths and tile prefix sums of up to
+  // kMaxSeqs sequences, the key-split merge statistics and the hand-off words
+  static constexpr int kLdsFixed = kMaxSeqs * 4 + (kMaxSeqs + 1) * 4 + kConsumers * 2 * kBlk * 4 + 512;
+  // the rest of the 160 KB: the cost prefix sums while the schedule is made,
+  // then the piece of the range's first segment until the range's last tile
+  static constexpr int kPieceLds = (160 * 1024 - kStages * kStage - kLdsFixed) / 16 * 16;
+  static_assert(kPieceLds >= (kMaxSeqs + 1) * 4, "LDS budget");
   static_assert(kConsumers * 64 * D <= kStage, "key-split merge scratch fits in a stage");
   static_assert(kNKB >= 2, "key blocks are processed in pairs");
 };
@@ -459,15 +465,22 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
 
 // TREE: the draft region obeys per-token draft-mask words instead of the
 // chain mask.  PAGED: the KV cache is a pool of pages found through a block
-// table.
-template <int ELT, int D, bool TREE, bool PAGED>
+// table.  HOLD (launches whose units have at most two 16-row blocks): each
+// range is streamed in order, and the piece of its first segment is held in
+// LDS until the range's last tile.
+template <int ELT, int D, bool TREE, bool PAGED, bool HOLD>
 __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   constexpr bool W16 = ELT != kF32;   // 16-bit elements
   using C = Cfg<W16, D>;
   __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
   __shared__ uint32_t seqs[kMaxSeqs];     // packed (T, c) of every sequence of the launch
   __shared__ int pref[kMaxSeqs + 1];      // tiles per KV head of the sequences before b
-  __shared__ int cpref[kMaxSeqs + 1];     // cost of one KV head's tiles of the sequences before b
+  // the cost of one KV head's tiles of the sequences before b; with HOLD it
+  // shares its LDS with the held piece (O rows, then the rows' max and sum),
+  // which is written only once the schedule has been made
+  __shared__ __attribute__((aligned(16))) char piece_lds[HOLD ? C::kPieceLds : 16];
+  __shared__ int cpref_own[HOLD ? 1 : kMaxSeqs + 1];
+  int* const cpref = HOLD ? reinterpret_cast<int*>(piece_lds) : cpref_own;
   __shared__ float mst[kConsumers][2][kBlk];   // key-split merge: max and sum of each wave's rows
   __shared__ int sh_flag[2];              // "this piece completed its unit", for the two pieces
   __shared__ int sh_share[2][4];          // unit, qf, ql, slot_first of the units of tiles g0 and g1 - 1
@@ -552,10 +565,9 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // ---- prologue, by wave 0 alone while the other waves wait at one
   // barrier (every wave doing it was issue-bound): the lengths, tile and cost
   // prefix sums into LDS, then this workgroup's range [g0, g1) and its first
-  // tile.  Lane l owns the contiguous sequences [l per, (l + 1) per).  If the
-  // range's last tile lies in a unit that starts inside the range and
-  // continues past it, that last segment [s_last, g1) is streamed first,
-  // then [g0, s_last).
+  // tile.  Lane l owns the contiguous sequences [l per, (l + 1) per).  The
+  // range is streamed in order, except that without HOLD a cut unit at its
+  // end is streamed first (below).
   __shared__ int sh_sched[12];
   if (wave == 0) {
     const int per = (B + 63) / 64;
@@ -597,12 +609,20 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     if (pid < sc.Pe) {
       g0 = sc.range_begin(pid);
       g1 = sc.range_begin(pid + 1);
-      first = locate(g1 - 1);
-      s_last = g1 - 1 - first.j;
-      const bool rotated = s_last > g0 && first.j < seq_tiles<C>(first.s) - 1;
-      nL = rotated ? g1 - s_last : 0;    // tiles of the rotated segment
-      if (rotated) first.j = 0;
-      else first = locate(g0);
+      if constexpr (HOLD) {
+        first = locate(g0);
+      } else {
+        // If the range's last tile lies in a unit that starts inside the
+        // range and continues past it, that last segment [s_last, g1) is
+        // streamed first, then [g0, s_last): its piece is then stored early
+        // and merged after the loop without holding the launch's end up.
+        first = locate(g1 - 1);
+        s_last = g1 - 1 - first.j;
+        const bool rotated = s_last > g0 && first.j < seq_tiles<C>(first.s) - 1;
+        nL = rotated ? g1 - s_last : 0;    // tiles of the rotated segment
+        if (rotated) first.j = 0;
+        else first = locate(g0);
+      }
     }
     if (lane == 0) {
       sh_sched[0] = total;
@@ -757,6 +777,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   int R = 0, n_rbp = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
   bool active = false, row_valid = false;
   uint64_t tmask = 0;   // (tree drafts) this lane's row: bit k = sees draft key l_ctx + k
+  // (tree drafts) the row's mask word of the current segment's unit and of
+  // the next segment's, loaded with that segment's Q: a load issued at the
+  // unit's start would be waited for inside the pair loop, and that wait
+  // would cover the Q prefetch and the stores issued before it
+  uint64_t tm_r = 0, tm_n = 0;
   // x / g for a row 0 <= x < 128 of a unit, by a float reciprocal: exact
   // there, as (x + 1/2) / g lies at least 1 / (2 g) from an integer
   const float inv_g = 1.f / (float)g;
@@ -780,14 +805,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       // every key below the sequence end passes the compare; the draft
       // keys are then filtered by the row's word
       vis = 0x7fffffff;
-      tmask = row_valid ? p.draft_mask[cu.b * p.C_max + tok] : 0;
+      tmask = tm_r;   // 0 for rows that are not valid
     } else {
       vis = row_valid ? l_ctx + tok : 0x7fffffff;   // last visible key of this lane's row
     }
   };
   // Q chunks of this lane's row for the unit of cu (zero for invalid rows):
   // chunk 4J + lg of the row feeds the J-th score MFMA.  Consumers only.
-  auto load_q = [&](const Cursor& cu, u32x4* dst) {
+  auto load_q = [&](const Cursor& cu, u32x4* dst, uint64_t& mdst) {
     const int c = seq_c(cu.s);
     const int uR = c * g;
     const int n_rb = (uR + kBlk - 1) / kBlk;
@@ -802,6 +827,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 #pragma unroll
     for (int J = 0; J < C::kQJ; ++J)
       dst[J] = ok ? *reinterpret_cast<const u32x4*>(qrow + 16 * (4 * J + lg)) : u32x4{0u, 0u, 0u, 0u};
+    if constexpr (TREE) mdst = ok ? p.draft_mask[cu.b * p.C_max + tk] : 0;
   };
 
   // Publication of pieces (at most two per workgroup: its first and last
@@ -812,8 +838,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // where the last piece of a unit merges it.  The loop runs idle iterations
   // after the last tile until every piece is counted.
   struct Pub {
-    int state;   // 0 stored, 1 counted, 2 no piece
-    int unit, v;
+    int state;   // 0 stored, 1 counted, 2 no piece, 3 held in LDS
+    int unit, v, rows;
   };
 
   // ---- consumers.  Per-segment state of a lane: O^T blocks, running max
@@ -826,14 +852,15 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 #pragma unroll
   for (int J = 0; J < C::kQJ; ++J) qn[J] = u32x4{0u, 0u, 0u, 0u};
   float m_run = -INFINITY, l_lane = 0.f;
-  Pub pub0 = {2, 0, 0}, pub1 = {2, 0, 0};
+  Pub pub0 = {2, 0, 0, 0}, pub1 = {2, 0, 0, 0};
   int n_pub = 0;
-  // The consumer wave that counts piece k on its unit's arrival counter
-  // keeps the counter's previous value in cnt[k] (lane 0) and sets bit k of
-  // counted; both are read after the loop, so the atomic's return is never
-  // waited for inside it.
-  int cnt[2] = {0, 0};
+  // The consumer wave that counts piece k on its unit's arrival counter sets
+  // bit k of counted and keeps the counter's previous value in cnt[k] (lane
+  // 0); the last piece to arrive merges the unit after the loop.  (Reading
+  // the counter back after the loop instead costs one more round trip at the
+  // end of the range, which measured slower.)
   int counted = 0;
+  int cnt[2] = {0, 0};
   int ncb = 0;   // consumer barriers passed
   auto cbar = [&]() {
     ++ncb;
@@ -844,7 +871,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // The first unit's Q arrives through qn, so that qr is only ever written
   // from registers and the score MFMAs never wait for a load.  The producers
   // start at once: the Q loads need not go out before the first tile's.
-  if (!producer) load_q(first, qn);
+  if (!producer) load_q(first, qn, tm_n);
   if (producer) {
     // Producer pair grp streams the tiles v = grp, grp + 2, ... of the
     // workgroup's order into stage grp: it waits until all consumers have
@@ -910,10 +937,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
 #pragma unroll
   for (int J = 0; J < C::kQJ; ++J) asm volatile("" : "+v"(qr[J])::"memory");
+  if constexpr (TREE) {
+    tm_r = tm_n;
+    asm volatile("" : "+v"(tm_r)::"memory");
+  }
   {
     int v1;
     const Cursor c1 = next_segment(first, 0, v1);
-    if (v1 < count) load_q(c1, qn);   // the second segment's Q
+    if (v1 < count) load_q(c1, qn, tm_n);   // the second segment's Q
   }
   pad_rows(ctid, kCThreads);   // while the first tile streams in
   Cursor cur = first;                  // cursor of the tile being computed
@@ -926,6 +957,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   float pend_inv = 0.f, pend_lse = 0.f;
 
   for (int v = 0;; ++v) {
+    // (a held piece is stored at iteration count - 1, so no piece is held here)
     if (v >= count && pub0.state != 0 && pub1.state != 0 && !pend) break;
     if (pend && pend_ok) {
       const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
@@ -958,6 +990,30 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       for (int db = 0; db < C::kDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     pend = false;
+    if (HOLD && pub0.state == 3 && v == pub0.v) {
+      // the held piece (the first segment's, slot 2 pid) goes out now, while
+      // the range's last tile streams in; it is counted two iterations later
+      cbar();   // every wave has written its slice of it
+      const __amdgpu_buffer_rsrc_t ws_o_rsrc = __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
+      const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
+          __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
+      const float* po = reinterpret_cast<const float*>(piece_lds);
+      const int rows = pub0.rows, row0 = 2 * pid * p.Rcap;
+      for (int idx = ctid; idx < rows * (D / 4); idx += kCThreads) {
+        const int r = idx / (D / 4);
+        const int d4 = idx - r * (D / 4);
+        const float l = po[rows * D + 2 * r + 1];
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(i32x4, *reinterpret_cast<const f32x4*>(po + r * D + 4 * d4) * (l > 0.f ? 1.f / l : 0.f)),
+            ws_o_rsrc, ((row0 + r) * D + 4 * d4) * 4, 0, kDeviceCoherent);
+      }
+      for (int r = ctid; r < rows; r += kCThreads) {
+        const float m = po[rows * D + 2 * r], l = po[rows * D + 2 * r + 1];
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, l > 0.f ? (m + log2f(l)) * kLn2 : -INFINITY),
+                                              ws_lse_rsrc, (row0 + r) * 4, 0, kDeviceCoherent);
+      }
+      pub0.state = 0;
+    }
     const bool due0 = pub0.state == 0 && v >= pub0.v + 2;
     const bool due1 = pub1.state == 0 && v >= pub1.v + 2;
     if (due0 || due1) {
@@ -1170,6 +1226,10 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       for (int J = 0; J < C::kQJ; ++J) qr[J] = qn[J];
 #pragma unroll
       for (int J = 0; J < C::kQJ; ++J) asm volatile("" : "+v"(qr[J])::"memory");
+      if constexpr (TREE) {
+        tm_r = tm_n;
+        asm volatile("" : "+v"(tm_r)::"memory");
+      }
       // the Q of the segment after next is loaded now, right after qn was
       // read, and before this segment's stores
       {
@@ -1178,7 +1238,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         if (v1 < count) {
           int v2;
           const Cursor c2 = next_segment(c1, v1, v2);
-          if (v2 < count) load_q(c2, qn);
+          if (v2 < count) load_q(c2, qn, tm_n);
         }
       }
       // ---- combine the key-split states of each row block in one LDS
@@ -1188,6 +1248,18 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       float fm = m_run, fl = row_sum(l_lane);   // this lane's row: max (log2 units) and sum
       const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
       const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
+      const int unit_first = gt - j;                 // global index of the unit's tile 0
+      const bool whole = seg_g == unit_first && j == n - 1;
+      // The piece of the range's first segment is held in LDS and stored
+      // only at the range's last tile, when it fits there and more tiles
+      // follow: stores issued while the range's tiles stream in slow the rest
+      // of the stream down, stores late in it much less.  It is written by
+      // the key-split merge below (units of one or two row blocks), not yet
+      // normalised: O rows, then (max, sum) per row.  (Those units' waves
+      // pass consumer barriers at each unit end, so by then the cost sums
+      // that share the LDS are no longer read.)
+      const bool hold =
+          HOLD && !whole && seg_g == g0 && v + 1 < count && nks > 1 && R * (D + 2) * 4 <= C::kPieceLds;
       if (nks > 1) {
         char* merge_lds = smem + st * C::kStage;
         cbar();   // every consumer is done with this tile's stage
@@ -1233,7 +1305,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
                 }
               }
               o[db] = acc;
+              if (hold && row_valid)
+                *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(piece_lds) + row * D + 16 * db + 4 * lg) = acc;
             }
+          }
+          if (hold && row_valid && kslot == 0 && lg == 0) {
+            float* ps = reinterpret_cast<float*>(piece_lds) + R * D + 2 * row;
+            ps[0] = M;
+            ps[1] = L;
           }
         }
       }
@@ -1241,8 +1320,6 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 
       // ---- this wave's slice of the result, stored at the top of the next
       // iteration: the whole unit (final result) or a piece of it
-      const int unit_first = gt - j;                 // global index of the unit's tile 0
-      const bool whole = seg_g == unit_first && j == n - 1;
       pend = true;
       pend_whole = whole;
       pend_ok = active && row_valid;
@@ -1255,6 +1332,18 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         q.state = 0;
         q.unit = b * Hkv + kvh;
         q.v = v + 1;   // the iteration that stores it
+        q.rows = R;
+        // The piece of the range's first segment is held in LDS and stored
+        // only at the range's last tile, when it fits there and more tiles
+        // follow: stores issued while the range's tiles stream in slow the
+        // rest of the stream down (measured), stores late in it much less.
+        // (Units with one or two row blocks: their waves pass consumer
+        // barriers at each unit end, so the cost sums are no longer read.)
+        if (hold) {
+          pend_ok = false;   // written to LDS by the key-split merge above
+          q.state = 3;
+          q.v = count - 1;   // the iteration that stores it
+        }
         if (n_pub == 0) pub0 = q;
         else pub1 = q;
         ++n_pub;
@@ -1360,6 +1449,9 @@ Plan make_plan(const specmoe_verify_desc* d) {
 template <int ELT, int D, bool TREE, bool PAGED>
 void launch(Params p, const Plan& pl, hipStream_t stream) {
   using C = Cfg<ELT != kF32, D>;
+  // units of at most two 16-row blocks whose piece fits the LDS left beside
+  // the stages hold their range's first piece there
+  const bool hold = p.Rcap <= 2 * kBlk && p.Rcap * (D + 2) * 4 <= C::kPieceLds;
   const int B = p.B;
   // batches beyond kMaxSeqs sequences run as consecutive launches on the stream
   for (int b0 = 0; b0 < B; b0 += kMaxSeqs) {
@@ -1378,7 +1470,8 @@ void launch(Params p, const Plan& pl, hipStream_t stream) {
     if (TREE) s.draft_mask = p.draft_mask + (size_t)b0 * p.C_max;
     s.out = p.out + (size_t)b0 * p.C_max * p.Hq * D;
     s.lse = p.lse + (size_t)b0 * p.C_max * p.Hq;
-    hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    if (hold) hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED, true>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    else hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED, false>), dim3(pl.P), dim3(kThreads), 0, stream, s);
   }
 }
 
