@@ -300,6 +300,13 @@ __device__ __forceinline__ int seq_tiles(uint32_t s) {
 // HBM stream lasts, so workgroups get equal cost rather than equal tiles.
 constexpr int kTileCost = 6;
 __device__ __forceinline__ int tile_cost(uint32_t s, int g) { return kTileCost + (seq_c(s) * g + kBlk - 1) / kBlk; }
+// Extra cost of a unit's start (its first tile): a workgroup pays at every
+// unit end for the merge of the key-split states, the result's stores and a
+// first tile that is mostly partial, so ranges that cross more unit
+// boundaries get fewer tiles.
+constexpr int kUnitCost = 4;
+// cost of one unit (one KV head) of a sequence: its tiles, plus the unit start
+__device__ __forceinline__ int unit_cost(int n, int w) { return n > 0 ? n * w + kUnitCost : 0; }
 
 // floor(a / b) for 0 <= a < 2^53 and 0 < b < 2^53: the rounded double
 // quotient is within one of it, and one exact integer step corrects it
@@ -313,22 +320,25 @@ __device__ __forceinline__ long long div_floor(long long a, long long b) {
 }
 
 // Tile schedule shared by every workgroup of a launch.  The tiles of all
-// units form one list [0, N) in (sequence, KV head, tile) order; tile t of
-// sequence b starts at cost Hkv cpref[b] + (t - Hkv pref[b]) w_b, w_b its
-// sequence's tile cost, out of Wt in all.  Range q holds the tiles whose start
-// cost lies in [q Wt / Pe, (q + 1) Wt / Pe).  With Pe <= Wt / max_b w_b no
-// range is empty, since consecutive tile starts are at most max_b w_b apart.
+// units form one list [0, N) in (sequence, KV head, tile) order; tile j of
+// unit kvh of sequence b starts at cost Hkv cpref[b] + kvh U_b + (j > 0 ?
+// S + j w_b : 0), w_b its sequence's tile cost, S the unit-start cost and
+// U_b = n_b w_b + S a unit's cost, out of Wt in all.  Range q holds the tiles
+// whose start cost lies in [q Wt / Pe, (q + 1) Wt / Pe).  With Pe <= Wt /
+// max_b (w_b + S) no range is empty, since consecutive tile starts are at
+// most max_b (w_b + S) apart.
 struct Sched {
   int N, Pe, B, Hkv, g;
-  bool uni;                 // every tile costs the same: the same ranges, found without a search
+  bool uni;                 // every tile costs the same and S = 0: the same ranges, found without a search
   long long Wt;
   const uint32_t* seqs;     // packed lengths per sequence
   const int* pref;          // tiles per KV head of the sequences before b
-  const int* cpref;         // cost of the tiles of one KV head of the sequences before b
-  // range of the tile at offset off = kvh * n + j of sequence b
-  __device__ int owner(int b, int off) const {
-    if (uni) return (int)div_floor((long long)(Hkv * pref[b] + off) * Pe, N);
-    const long long c = (long long)Hkv * cpref[b] + (long long)off * tile_cost(seqs[b], g);
+  const int* cpref;         // cost of the units of one KV head of the sequences before b
+  // range of tile j of unit kvh of sequence b (n tiles per unit)
+  __device__ int owner(int b, int kvh, int j, int n) const {
+    if (uni) return (int)div_floor((long long)(Hkv * pref[b] + kvh * n + j) * Pe, N);
+    const int w = tile_cost(seqs[b], g);
+    const long long c = (long long)Hkv * cpref[b] + (long long)kvh * unit_cost(n, w) + (j > 0 ? kUnitCost + j * w : 0);
     return (int)div_floor(c * Pe, Wt);
   }
   // first tile of range q (N for q = Pe); every lane of the wave takes part
@@ -347,9 +357,21 @@ struct Sched {
     const int i2 = min(base + lane, B);
     const unsigned long long m2 = __ballot(lane < step && cpref[i2] * hp <= X);
     const int b = __builtin_amdgcn_readfirstlane(base + 63 - __builtin_clzll(m2));
-    const long long den = (long long)tile_cost(seqs[b], g) * Pe;
-    const long long off = div_floor(X - cpref[b] * hp + den - 1, den);   // <= Hkv tiles(b)
-    return Hkv * pref[b] + (int)off;
+    const int n = pref[b + 1] - pref[b];   // tiles per unit of sequence b
+    const int w = tile_cost(seqs[b], g);
+    // the unit of sequence b whose cost interval holds X, then the first of
+    // its tiles that starts at or after X (or the next unit's first tile)
+    const long long rem = X - cpref[b] * hp;   // >= 0
+    const long long U = (long long)unit_cost(n, w) * Pe;
+    const int kvh = (int)div_floor(rem, U);
+    const long long rem2 = rem - kvh * U;
+    int j = 0;
+    if (rem2 > 0) {
+      const long long den = (long long)w * Pe;
+      j = (int)div_floor(rem2 - (long long)kUnitCost * Pe + den - 1, den);
+      j = j < 1 ? 1 : j;   // <= n: then the next unit's first tile
+    }
+    return Hkv * pref[b] + kvh * n + j;
   }
 };
 
@@ -552,14 +574,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   sc.cpref = cpref;
   // every tile costs at most w_hi, so with at most Wt / w_hi ranges (and at
   // least one when there are tiles) no range is empty
-  const int w_hi = kTileCost + (p.C_max * g + kBlk - 1) / kBlk;
+  const int w_hi = kTileCost + (p.C_max * g + kBlk - 1) / kBlk + kUnitCost;
   auto set_totals = [&](int tiles_per_head, int cost_per_head) {
     sc.N = tiles_per_head * Hkv;   // tiles of all units (< 2^30, host check)
     sc.Wt = (long long)Hkv * cost_per_head;
     long long pe = div_floor(sc.Wt, w_hi);
     if (pe < 1) pe = sc.N > 0 ? 1 : 0;
     sc.Pe = pe < p.P ? (int)pe : p.P;
-    sc.uni = sc.Wt == (long long)sc.N * w_hi;
+    sc.uni = kUnitCost == 0 && sc.Wt == (long long)sc.N * w_hi;
   };
 
   // ---- prologue, by wave 0 alone while the other waves wait at one
@@ -578,7 +600,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       const uint32_t s = load_seq(p, b);
       seqs[b] = s;
       my_tiles += seq_tiles<C>(s);
-      my_cost += seq_tiles<C>(s) * tile_cost(s, g);
+      my_cost += unit_cost(seq_tiles<C>(s), tile_cost(s, g));
     }
     const int incl = wave_scan(my_tiles), cincl = wave_scan(my_cost);
     const int total = __builtin_amdgcn_readlane(incl, 63);
@@ -588,7 +610,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       pref[b] = run;
       cpref[b] = crun;
       run += seq_tiles<C>(seqs[b]);
-      crun += seq_tiles<C>(seqs[b]) * tile_cost(seqs[b], g);
+      crun += unit_cost(seq_tiles<C>(seqs[b]), tile_cost(seqs[b], g));
     }
     if (lane == 63) {
       pref[B] = total;
@@ -922,8 +944,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       const int t = k == 0 ? g0 : g1 - 1;
       const Cursor cu = locate(t);
       const int n = seq_tiles<C>(cu.s);
-      const int qf = sc.owner(cu.b, cu.kvh * n);
-      const int ql = sc.owner(cu.b, cu.kvh * n + n - 1);
+      const int qf = sc.owner(cu.b, cu.kvh, 0, n);
+      const int ql = sc.owner(cu.b, cu.kvh, n - 1, n);
       const int slot_first = 2 * qf + (sc.range_begin(qf) < t - cu.j ? 1 : 0);   // whole wave: a ballot search
       if (lane == 0) {
         sh_share[k][0] = cu.b * Hkv + cu.kvh;
@@ -1426,7 +1448,7 @@ int validate_desc(const specmoe_verify_desc* d) {
   const int64_t tile = key_tile(d->dtype, d->D);
   if ((int64_t)kMaxSeqs * d->Hkv * ((d->S_max + tile - 1) / tile) >= ((int64_t)1 << 30)) return SPECMOE_ERR_SHAPE;
   // the per-KV-head tile cost prefix of the schedule fits in 32 bits
-  const int64_t w_hi = kTileCost + (d->C_max * g + kBlk - 1) / kBlk;
+  const int64_t w_hi = kTileCost + (d->C_max * g + kBlk - 1) / kBlk + kUnitCost;
   if ((int64_t)kMaxSeqs * ((d->S_max + tile - 1) / tile) * w_hi >= ((int64_t)1 << 31)) return SPECMOE_ERR_SHAPE;
   return SPECMOE_OK;
 }
