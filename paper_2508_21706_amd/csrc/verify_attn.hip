@@ -596,16 +596,21 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int b_lo = min(lane * per, B);
     const int b_hi = min(b_lo + per, B);
     int my_tiles = 0, my_cost = 0;   // sums < 2^31 (host check)
+    uint32_t my_s = 0;               // (B <= 64) the packed lengths of sequence lane
     for (int b = b_lo; b < b_hi; ++b) {
       const uint32_t s = load_seq(p, b);
       seqs[b] = s;
+      my_s = s;
       my_tiles += seq_tiles<C>(s);
       my_cost += unit_cost(seq_tiles<C>(s), tile_cost(s, g));
     }
     const int incl = wave_scan(my_tiles), cincl = wave_scan(my_cost);
     const int total = __builtin_amdgcn_readlane(incl, 63);
     const int ctotal = __builtin_amdgcn_readlane(cincl, 63);
-    int run = incl - my_tiles, crun = cincl - my_cost;
+    // exclusive prefixes: pref[b_lo] and cpref[b_lo] (the totals in lanes
+    // without sequences)
+    const int ex = incl - my_tiles, cex = cincl - my_cost;
+    int run = ex, crun = cex;
     for (int b = b_lo; b < b_hi; ++b) {
       pref[b] = run;
       cpref[b] = crun;
@@ -626,24 +631,65 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       sh_flag[lane] = 0;
     }
     set_totals(total, ctotal);
+    // With at most 64 sequences lane l holds sequence l (one per lane), and
+    // with ex = pref[min(l, B)], cex = cpref[min(l, B)] the searches below
+    // run on registers and ballots instead of LDS round trips: the same
+    // results as Sched::range_begin and locate.
+    const bool in_regs = B <= 64;
+    auto range_begin_w0 = [&](int q) {
+      if (!in_regs || q >= sc.Pe || sc.uni) return sc.range_begin(q);
+      const long long X = (long long)q * sc.Wt, hp = (long long)Hkv * sc.Pe;
+      // lane 0 (cex = 0) always passes, lanes from B on (cex = ctotal, and
+      // ctotal hp = Pe Wt > X) never do
+      const unsigned long long m = __ballot((long long)cex * hp <= X);
+      const int b = 63 - __builtin_clzll(m);
+      const int n = __builtin_amdgcn_readlane(my_tiles, b);
+      const int w = tile_cost((uint32_t)__builtin_amdgcn_readlane((int)my_s, b), g);
+      const long long rem = X - (long long)__builtin_amdgcn_readlane(cex, b) * hp;
+      const long long U = (long long)unit_cost(n, w) * sc.Pe;
+      const int kvh = (int)div_floor(rem, U);
+      const long long rem2 = rem - kvh * U;
+      int j = 0;
+      if (rem2 > 0) {
+        const long long den = (long long)w * sc.Pe;
+        j = (int)div_floor(rem2 - (long long)kUnitCost * sc.Pe + den - 1, den);
+        j = j < 1 ? 1 : j;
+      }
+      return Hkv * __builtin_amdgcn_readlane(ex, b) + kvh * n + j;
+    };
+    auto locate_w0 = [&](int t) {
+      if (!in_regs) return locate(t);
+      // lane 0 (ex = 0) always passes, lanes from B on (ex = total > t / Hkv
+      // for t < N) never do
+      const unsigned long long m = __ballot(ex <= t / Hkv);
+      const int b = 63 - __builtin_clzll(m);
+      Cursor cu;
+      cu.b = b;
+      cu.s = (uint32_t)__builtin_amdgcn_readlane((int)my_s, b);
+      const int n = seq_tiles<C>(cu.s);
+      const int off = t - Hkv * __builtin_amdgcn_readlane(ex, b);
+      cu.kvh = off / n;
+      cu.j = off - cu.kvh * n;
+      return cu;
+    };
     int g0 = 0, g1 = 0, nL = 0, s_last = 0;
     Cursor first = {0, 0, 0, 0u};
     if (pid < sc.Pe) {
-      g0 = sc.range_begin(pid);
-      g1 = sc.range_begin(pid + 1);
+      g0 = range_begin_w0(pid);
+      g1 = range_begin_w0(pid + 1);
       if constexpr (HOLD) {
-        first = locate(g0);
+        first = locate_w0(g0);
       } else {
         // If the range's last tile lies in a unit that starts inside the
         // range and continues past it, that last segment [s_last, g1) is
         // streamed first, then [g0, s_last): its piece is then stored early
         // and merged after the loop without holding the launch's end up.
-        first = locate(g1 - 1);
+        first = locate_w0(g1 - 1);
         s_last = g1 - 1 - first.j;
         const bool rotated = s_last > g0 && first.j < seq_tiles<C>(first.s) - 1;
         nL = rotated ? g1 - s_last : 0;    // tiles of the rotated segment
         if (rotated) first.j = 0;
-        else first = locate(g0);
+        else first = locate_w0(g0);
       }
     }
     if (lane == 0) {
