@@ -115,6 +115,8 @@ constexpr int kDeviceCoherent = 16;   // SC1
 // reused (the partial results, the output being written); with the default
 // policy the whole launch ran 6-11% slower.
 constexpr int kStreaming = 2;
+// kernel variants (template argument MODE)
+constexpr int kModePlain = 0, kModeHold = 1, kModeNt = 2;
 constexpr int kBufferFormat = 0x00020000;   // raw 32-bit buffer descriptor word 3
 
 struct Params {
@@ -390,7 +392,7 @@ struct Cursor {
 // items of both units form one list, and each thread takes three items per
 // round and issues all their loads before it waits, so the two units' loads
 // go out together.  Unit u is described by e_u = {unit, qf, ql, slot_first}.
-template <int D>
+template <int D, bool NT>
 __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seqs, int ctid, const int* e_a,
                                          const int* e_b, bool has_a, bool has_b) {
   const __amdgpu_buffer_rsrc_t ws_o_rsrc = __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
@@ -475,8 +477,15 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
     for (int it = 0; it < kItems; ++it) {
       if (base + it * kCThreads >= n_items) continue;
       // (z = 0: a row that sees no key in any piece)
-      *reinterpret_cast<f32x4*>(p.out + orow[it] * D + d0[it]) = acc[it] * (z[it] > 0.f ? 1.f / z[it] : 0.f);
-      if (d0[it] == 0) p.lse[orow[it]] = z[it] > 0.f ? m[it] + logf(z[it]) : -INFINITY;
+      const f32x4 res = acc[it] * (z[it] > 0.f ? 1.f / z[it] : 0.f);
+      const float res_lse = z[it] > 0.f ? m[it] + logf(z[it]) : -INFINITY;
+      if constexpr (NT) {
+        __builtin_nontemporal_store(res, reinterpret_cast<f32x4*>(p.out + orow[it] * D + d0[it]));
+        if (d0[it] == 0) __builtin_nontemporal_store(res_lse, p.lse + orow[it]);
+      } else {
+        *reinterpret_cast<f32x4*>(p.out + orow[it] * D + d0[it]) = res;
+        if (d0[it] == 0) p.lse[orow[it]] = res_lse;
+      }
     }
   }
   if (ctid == 0) {   // ready for the next call
@@ -487,11 +496,15 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
 
 // TREE: the draft region obeys per-token draft-mask words instead of the
 // chain mask.  PAGED: the KV cache is a pool of pages found through a block
-// table.  HOLD (launches whose units have at most two 16-row blocks): each
-// range is streamed in order, and the piece of its first segment is held in
-// LDS until the range's last tile.
-template <int ELT, int D, bool TREE, bool PAGED, bool HOLD>
+// table.  MODE kModeHold (launches whose units have at most two 16-row
+// blocks): each range is streamed in order, and the piece of its first
+// segment is held in LDS until the range's last tile.  MODE kModeNt: results
+// are stored with the non-temporal policy (launches with many units per
+// workgroup and a large output).
+template <int ELT, int D, bool TREE, bool PAGED, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
+  constexpr bool HOLD = MODE == kModeHold;
+  constexpr bool NT = MODE == kModeNt;
   constexpr bool W16 = ELT != kF32;   // 16-bit elements
   using C = Cfg<W16, D>;
   __shared__ __attribute__((aligned(16))) char smem[kStages * C::kStage];
@@ -1032,10 +1045,18 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
       if (pend_whole) {
         float* dst = p.out + (size_t)pend_row * D;
-        if (kslot == 0 && lg == 0) p.lse[pend_row] = pend_lse;
+        if (kslot == 0 && lg == 0) {
+          if constexpr (NT) __builtin_nontemporal_store(pend_lse, p.lse + pend_row);
+          else p.lse[pend_row] = pend_lse;
+        }
 #pragma unroll
         for (int db = 0; db < C::kDB; ++db)
-          if (db >= d_lo && db < d_hi) *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = o[db] * pend_inv;
+          if (db >= d_lo && db < d_hi) {
+            if constexpr (NT)
+              __builtin_nontemporal_store(o[db] * pend_inv, reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg));
+            else
+              *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = o[db] * pend_inv;
+          }
       } else {
         // read by another workgroup, possibly on another XCD
         const __amdgpu_buffer_rsrc_t ws_o_rsrc =
@@ -1437,7 +1458,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   cbar();
   {
     const int f0 = sh_flag[0], f1 = sh_flag[1];
-    if (f0 || f1) merge_units<D>(p, seqs, ctid, sh_share[f0 ? f0 - 1 : 0], sh_share[f1 ? f1 - 1 : 0], f0 != 0, f1 != 0);
+    if (f0 || f1)
+      merge_units<D, NT>(p, seqs, ctid, sh_share[f0 ? f0 - 1 : 0], sh_share[f1 ? f1 - 1 : 0], f0 != 0, f1 != 0);
   }
   report_give_up(gave_up);
 }
@@ -1514,6 +1536,17 @@ Plan make_plan(const specmoe_verify_desc* d) {
   return pl;
 }
 
+// Results (out and lse) are stored write-back, except in launches with both
+// many units per workgroup (at least kNtUnitsPerWg) and a large output (at
+// least kNtOutBytes), where the workgroups store results many times while the
+// K/V stream runs: there the non-temporal policy measured faster (B = 256, 8
+// KV heads, 16-33 MB of output: 2-7%; B = 128, 10.5 MB: 1.4%), while launches
+// with fewer, larger units (ragged chunks, tree drafts, B = 64) or a small
+// output (one-token decode) were 1-5% slower with it.  Launches that hold
+// their first piece in LDS keep that variant.
+constexpr int kNtUnitsPerWg = 4;
+constexpr size_t kNtOutBytes = (size_t)8 << 20;
+
 template <int ELT, int D, bool TREE, bool PAGED>
 void launch(Params p, const Plan& pl, hipStream_t stream) {
   using C = Cfg<ELT != kF32, D>;
@@ -1538,8 +1571,14 @@ void launch(Params p, const Plan& pl, hipStream_t stream) {
     if (TREE) s.draft_mask = p.draft_mask + (size_t)b0 * p.C_max;
     s.out = p.out + (size_t)b0 * p.C_max * p.Hq * D;
     s.lse = p.lse + (size_t)b0 * p.C_max * p.Hq;
-    if (hold) hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED, true>), dim3(pl.P), dim3(kThreads), 0, stream, s);
-    else hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED, false>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    const bool nt = s.B * p.Hkv >= kNtUnitsPerWg * pl.P &&
+                    (size_t)s.B * p.C_max * p.Hq * (D + 1) * sizeof(float) >= kNtOutBytes;
+    if (hold)
+      hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED, kModeHold>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    else if (nt)
+      hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED, kModeNt>), dim3(pl.P), dim3(kThreads), 0, stream, s);
+    else
+      hipLaunchKernelGGL((verify_attn_kernel<ELT, D, TREE, PAGED, kModePlain>), dim3(pl.P), dim3(kThreads), 0, stream, s);
   }
 }
 
