@@ -849,12 +849,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 
   // ---- consumer roles for the unit of cursor cu.  Rows are cut into
   // n_rb 16-row blocks; consumer wave wc takes row block rb = wc % n_rbp, and
-  // the nks = 8 / n_rbp waves of a row block share every tile's key blocks:
-  // wave kslot takes the pairs (kb, kb + nks) for kb = kslot, kslot + 2 nks,
-  // ...  (nks <= kNKB / 2, so every wave has whole pairs).  n_rbp is 1 or 2
-  // for one or two row blocks (four waves per block), else 8: from three
-  // blocks on, a wave computes its block's whole tile, which is cheaper than
-  // merging the waves' partial states at the end of every unit.
+  // the nks waves of a row block (its key slots) share every tile's key
+  // blocks: wave kslot takes the pairs (kb, kb + nks) for kb = kslot,
+  // kslot + 2 nks, ...  (nks <= kNKB / 2, so every wave has whole pairs).
+  // One row block: four waves (nks = 4).  Two: two waves per block (the
+  // merge of the waves' partial states at every unit end costs more than the
+  // compute that two more waves per block would take over), four waves idle.
+  // From three blocks on (n_rbp = 8), a wave computes its block's whole
+  // tile, which is cheaper than merging at the end of every unit.
   int R = 0, n_rbp = 1, nks = 1, rb = 0, kslot = 0, l_ctx = 0, row = 0, tok = 0, vis = 0;
   bool active = false, row_valid = false;
   uint64_t tmask = 0;   // (tree drafts) this lane's row: bit k = sees draft key l_ctx + k
@@ -868,6 +870,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   const float inv_g = 1.f / (float)g;
   auto div_g = [&](int x) { return (int)(((float)x + 0.5f) * inv_g); };
   auto rbp_shift = [&](int n_rb) { return n_rb <= 1 ? 0 : n_rb <= 2 ? 1 : 3; };   // log2 n_rbp
+  // waves that share a row block's tiles (key slots)
+  auto key_slots = [&](int n_rb, int sh) { return n_rb == 2 ? 2 : min(kConsumers >> sh, C::kNKB / 2); };
   auto roles = [&](const Cursor& cu) {
     const int c = seq_c(cu.s);
     R = c * g;
@@ -875,7 +879,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int n_rb = (R + kBlk - 1) / kBlk;
     const int sh = rbp_shift(n_rb);
     n_rbp = 1 << sh;
-    nks = min(kConsumers >> sh, C::kNKB / 2);   // consumers that share a row block
+    nks = key_slots(n_rb, sh);
     rb = producer ? 0 : wc & (n_rbp - 1);
     kslot = producer ? nks : wc >> sh;
     active = !producer && rb < n_rb && kslot < nks;
@@ -901,7 +905,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int rb_ = wc & ((1 << sh) - 1);
     const int ks_ = wc >> sh;
     const int row_ = rb_ * kBlk + lm;
-    const bool ok = rb_ < n_rb && ks_ < min(kConsumers >> sh, C::kNKB / 2) && row_ < uR;
+    const bool ok = rb_ < n_rb && ks_ < key_slots(n_rb, sh) && row_ < uR;
     const int tk = ok ? div_g(row_) : 0;
     const char* qrow =
         p.q + ((size_t)(cu.b * p.C_max + tk) * p.Hq + cu.kvh * g + (ok ? row_ - tk * g : 0)) * C::kRowBytes;
