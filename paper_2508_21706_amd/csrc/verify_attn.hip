@@ -176,6 +176,10 @@ struct Cfg {
   static constexpr int kPieceLds = (160 * 1024 - kStages * kStage - kLdsFixed) / 16 * 16;
   static_assert(kPieceLds >= (kMaxSeqs + 1) * 4, "LDS budget");
   static_assert(kConsumers * 64 * D <= kStage, "key-split merge scratch fits in a stage");
+  // the most (row block, key slot) regions a merge uses: one block with
+  // min(kConsumers, kNKB / 2) key slots, or two blocks with two each
+  static constexpr int kMergeRegions = kConsumers < kNKB / 2 ? kConsumers : kNKB / 2 > 4 ? kNKB / 2 : 4;
+  static_assert(kMergeRegions * 64 * D <= kLdsK, "key-split merge scratch stays in the K half of a stage");
   static_assert(kNKB >= 2, "key blocks are processed in pairs");
 };
 
@@ -779,9 +783,12 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // of its own row, and within a partial tile the lanes past its last row
   // re-read that row.  K loads that would start past the last row are not
   // issued: those slots keep whatever an earlier tile or merge left there,
-  // and the consumers mask the keys.  V rows are always loaded, so that a
-  // masked key (probability 0) always meets finite V values.  The two waves of a producer pair issue the K and V
-  // instructions of even and odd index.
+  // and the consumers mask the keys.  A masked key has probability 0 but
+  // must meet finite V values: the first tile of each stage loads every V
+  // slot (LDS starts undefined), later tiles skip the V loads past the last
+  // row too, whose slots then hold rows of an earlier tile (the key-split
+  // merge's scratch stays in the K half).  The two waves of a producer pair
+  // issue the K and V instructions of even and odd index.
   const int pw = wave & 1;
   // (paged) the pool pages of the tile of cu, one per lane of a producer
   // wave: lane l holds the page of the tile's l-th page (at most 33 of them:
@@ -799,7 +806,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     }
     return r;
   };
-  auto dma = [&](const Cursor& cu, int st, int pg) {
+  auto dma = [&](const Cursor& cu, int st, int pg, bool all_v) {
     const int T = seq_T(cu.s);
     const int hi = T - (seq_tiles<C>(cu.s) - 1 - cu.j) * C::kTileKeys;
     const int lo = hi > C::kTileKeys ? hi - C::kTileKeys : 0;
@@ -843,7 +850,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       if (i < C::kInstK && sl < C::kTileKeys * C::kSlotsK && (64 * i) / C::kSlotsK <= last)
         __builtin_amdgcn_global_load_lds(ksrc, (__attribute__((address_space(3))) void*)(kl + 1024 * i), 16, 0,
                                          kStreaming);
-      if (i < C::kInstV && sl < C::kTileKeys * C::kSlotsV)
+      if (i < C::kInstV && sl < C::kTileKeys * C::kSlotsV && (all_v || (64 * i) / C::kSlotsV <= last))
         __builtin_amdgcn_global_load_lds(vsrc, (__attribute__((address_space(3))) void*)(vl + 1024 * i), 16, 0,
                                          kStreaming);
     }
@@ -979,7 +986,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     for (; v < count; v += 2) {
       if (v >= 2) gave_up |= !wait_count(&empty_cnt[grp], kConsumers * (v >> 1), p.spin_limit);
       if (v == 1) gave_up |= !wait_count(&full_cnt[0], 2, p.spin_limit);
-      dma(cu, grp, pg);
+      dma(cu, grp, pg, v < 2);
       if constexpr (PAGED) {
         // the next tile's table entries ride the wait for this tile's loads
         if (v + 2 < count) {
