@@ -304,13 +304,15 @@ __device__ __forceinline__ int seq_tiles(uint32_t s) {
 // streaming the tile, plus one per 16-row block of the unit's c * g query
 // rows.  A unit with many rows can take longer on a tile than the tile's
 // HBM stream lasts, so workgroups get equal cost rather than equal tiles.
-constexpr int kTileCost = 6;
+// The weights follow measured tile times (ragged chunks, 1-7 row blocks:
+// 2.7, 3.1 and 3.3 us per tile for 1-2, 3-4 and 5-7 blocks).
+constexpr int kTileCost = 10;
 __device__ __forceinline__ int tile_cost(uint32_t s, int g) { return kTileCost + (seq_c(s) * g + kBlk - 1) / kBlk; }
 // Extra cost of a unit's start (its first tile): a workgroup pays at every
 // unit end for the merge of the key-split states, the result's stores and a
 // first tile that is mostly partial, so ranges that cross more unit
 // boundaries get fewer tiles.
-constexpr int kUnitCost = 4;
+constexpr int kUnitCost = 6;
 // cost of one unit (one KV head) of a sequence: its tiles, plus the unit start
 __device__ __forceinline__ int unit_cost(int n, int w) { return n > 0 ? n * w + kUnitCost : 0; }
 
