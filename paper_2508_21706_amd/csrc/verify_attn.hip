@@ -308,13 +308,24 @@ __device__ __forceinline__ int seq_tiles(uint32_t s) {
 // 2.7, 3.1 and 3.3 us per tile for 1-2, 3-4 and 5-7 blocks).
 constexpr int kTileCost = 10;
 __device__ __forceinline__ int tile_cost(uint32_t s, int g) { return kTileCost + (seq_c(s) * g + kBlk - 1) / kBlk; }
-// Extra cost of a unit's start (its first tile): a workgroup pays at every
-// unit end for the merge of the key-split states, the result's stores and a
-// first tile that is mostly partial, so ranges that cross more unit
-// boundaries get fewer tiles.
-constexpr int kUnitCost = 6;
-// cost of one unit (one KV head) of a sequence: its tiles, plus the unit start
-__device__ __forceinline__ int unit_cost(int n, int w) { return n > 0 ? n * w + kUnitCost : 0; }
+// Extra costs of a unit: at its start (a first tile that is mostly partial,
+// the switch of Q) and at its end (the result's stores and, for units of one
+// or two row blocks, the merge of the key-split states; charged after its
+// last tile), so ranges that cross more unit boundaries get fewer tiles.  A
+// range that starts inside a unit pays for that unit's end.  (Measured: on
+// B = 64 with chunks of 5 and 4 query heads per KV head a unit end holds a
+// workgroup ~1.6 us and its start ~0.6 us, against ~2.2 us per tile.)
+constexpr int kStartSplit = 3, kEndSplit = 9;   // units of one or two row blocks
+constexpr int kStartRest = 6, kEndRest = 0;     // larger units
+constexpr int kExtraMax = kStartSplit + kEndSplit > kStartRest + kEndRest ? kStartSplit + kEndSplit : kStartRest + kEndRest;
+__device__ __forceinline__ bool split_unit(uint32_t s, int g) { return seq_c(s) * g <= 2 * kBlk; }
+__device__ __forceinline__ int start_cost(uint32_t s, int g) { return split_unit(s, g) ? kStartSplit : kStartRest; }
+__device__ __forceinline__ int end_cost(uint32_t s, int g) { return split_unit(s, g) ? kEndSplit : kEndRest; }
+// cost of one unit (one KV head) of a sequence with packed lengths s: its n
+// tiles of cost w, its start and its end
+__device__ __forceinline__ int unit_cost(int n, int w, uint32_t s, int g) {
+  return n > 0 ? n * w + start_cost(s, g) + end_cost(s, g) : 0;
+}
 
 // floor(a / b) for 0 <= a < 2^53 and 0 < b < 2^53: the rounded double
 // quotient is within one of it, and one exact integer step corrects it
@@ -330,11 +341,11 @@ __device__ __forceinline__ long long div_floor(long long a, long long b) {
 // Tile schedule shared by every workgroup of a launch.  The tiles of all
 // units form one list [0, N) in (sequence, KV head, tile) order; tile j of
 // unit kvh of sequence b starts at cost Hkv cpref[b] + kvh U_b + (j > 0 ?
-// S + j w_b : 0), w_b its sequence's tile cost, S the unit-start cost and
-// U_b = n_b w_b + S a unit's cost, out of Wt in all.  Range q holds the tiles
-// whose start cost lies in [q Wt / Pe, (q + 1) Wt / Pe).  With Pe <= Wt /
-// max_b (w_b + S) no range is empty, since consecutive tile starts are at
-// most max_b (w_b + S) apart.
+// S_b + j w_b : 0), w_b its sequence's tile cost, S_b and E_b its unit-start
+// and unit-end costs and U_b = n_b w_b + S_b + E_b a unit's cost, out of Wt
+// in all.  Range q holds the tiles whose start cost lies in [q Wt / Pe, (q +
+// 1) Wt / Pe).  With Pe <= Wt / max_b (w_b + S_b + E_b) no range is empty,
+// since consecutive tile starts are at most max_b (w_b + S_b + E_b) apart.
 struct Sched {
   int N, Pe, B, Hkv, g;
   bool uni;                 // every tile costs the same and S = 0: the same ranges, found without a search
@@ -346,7 +357,8 @@ struct Sched {
   __device__ int owner(int b, int kvh, int j, int n) const {
     if (uni) return (int)div_floor((long long)(Hkv * pref[b] + kvh * n + j) * Pe, N);
     const int w = tile_cost(seqs[b], g);
-    const long long c = (long long)Hkv * cpref[b] + (long long)kvh * unit_cost(n, w) + (j > 0 ? kUnitCost + j * w : 0);
+    const long long c =
+        (long long)Hkv * cpref[b] + (long long)kvh * unit_cost(n, w, seqs[b], g) + (j > 0 ? start_cost(seqs[b], g) + j * w : 0);
     return (int)div_floor(c * Pe, Wt);
   }
   // first tile of range q (N for q = Pe); every lane of the wave takes part
@@ -370,14 +382,14 @@ struct Sched {
     // the unit of sequence b whose cost interval holds X, then the first of
     // its tiles that starts at or after X (or the next unit's first tile)
     const long long rem = X - cpref[b] * hp;   // >= 0
-    const long long U = (long long)unit_cost(n, w) * Pe;
+    const long long U = (long long)unit_cost(n, w, seqs[b], g) * Pe;
     const int kvh = (int)div_floor(rem, U);
     const long long rem2 = rem - kvh * U;
     int j = 0;
     if (rem2 > 0) {
       const long long den = (long long)w * Pe;
-      j = (int)div_floor(rem2 - (long long)kUnitCost * Pe + den - 1, den);
-      j = j < 1 ? 1 : j;   // <= n: then the next unit's first tile
+      j = (int)div_floor(rem2 - (long long)start_cost(seqs[b], g) * Pe + den - 1, den);
+      j = j < 1 ? 1 : j > n ? n : j;   // n: the next unit's first tile
     }
     return Hkv * pref[b] + kvh * n + j;
   }
@@ -596,14 +608,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   sc.cpref = cpref;
   // every tile costs at most w_hi, so with at most Wt / w_hi ranges (and at
   // least one when there are tiles) no range is empty
-  const int w_hi = kTileCost + (p.C_max * g + kBlk - 1) / kBlk + kUnitCost;
+  const int w_hi = kTileCost + (p.C_max * g + kBlk - 1) / kBlk + kExtraMax;
   auto set_totals = [&](int tiles_per_head, int cost_per_head) {
     sc.N = tiles_per_head * Hkv;   // tiles of all units (< 2^30, host check)
     sc.Wt = (long long)Hkv * cost_per_head;
     long long pe = div_floor(sc.Wt, w_hi);
     if (pe < 1) pe = sc.N > 0 ? 1 : 0;
     sc.Pe = pe < p.P ? (int)pe : p.P;
-    sc.uni = kUnitCost == 0 && sc.Wt == (long long)sc.N * w_hi;
+    sc.uni = kExtraMax == 0 && sc.Wt == (long long)sc.N * w_hi;
   };
 
   // ---- prologue, by wave 0 alone while the other waves wait at one
@@ -624,7 +636,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       seqs[b] = s;
       my_s = s;
       my_tiles += seq_tiles<C>(s);
-      my_cost += unit_cost(seq_tiles<C>(s), tile_cost(s, g));
+      my_cost += unit_cost(seq_tiles<C>(s), tile_cost(s, g), s, g);
     }
     const int incl = wave_scan(my_tiles), cincl = wave_scan(my_cost);
     const int total = __builtin_amdgcn_readlane(incl, 63);
@@ -637,7 +649,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       pref[b] = run;
       cpref[b] = crun;
       run += seq_tiles<C>(seqs[b]);
-      crun += unit_cost(seq_tiles<C>(seqs[b]), tile_cost(seqs[b], g));
+      crun += unit_cost(seq_tiles<C>(seqs[b]), tile_cost(seqs[b], g), seqs[b], g);
     }
     if (lane == 63) {
       pref[B] = total;
@@ -666,16 +678,17 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       const unsigned long long m = __ballot((long long)cex * hp <= X);
       const int b = 63 - __builtin_clzll(m);
       const int n = __builtin_amdgcn_readlane(my_tiles, b);
-      const int w = tile_cost((uint32_t)__builtin_amdgcn_readlane((int)my_s, b), g);
+      const uint32_t s_b = (uint32_t)__builtin_amdgcn_readlane((int)my_s, b);
+      const int w = tile_cost(s_b, g);
       const long long rem = X - (long long)__builtin_amdgcn_readlane(cex, b) * hp;
-      const long long U = (long long)unit_cost(n, w) * sc.Pe;
+      const long long U = (long long)unit_cost(n, w, s_b, g) * sc.Pe;
       const int kvh = (int)div_floor(rem, U);
       const long long rem2 = rem - kvh * U;
       int j = 0;
       if (rem2 > 0) {
         const long long den = (long long)w * sc.Pe;
-        j = (int)div_floor(rem2 - (long long)kUnitCost * sc.Pe + den - 1, den);
-        j = j < 1 ? 1 : j;
+        j = (int)div_floor(rem2 - (long long)start_cost(s_b, g) * sc.Pe + den - 1, den);
+        j = j < 1 ? 1 : j > n ? n : j;
       }
       return Hkv * __builtin_amdgcn_readlane(ex, b) + kvh * n + j;
     };
@@ -1536,7 +1549,7 @@ int validate_desc(const specmoe_verify_desc* d) {
   const int64_t tile = key_tile(d->dtype, d->D);
   if ((int64_t)kMaxSeqs * d->Hkv * ((d->S_max + tile - 1) / tile) >= ((int64_t)1 << 30)) return SPECMOE_ERR_SHAPE;
   // the per-KV-head tile cost prefix of the schedule fits in 32 bits
-  const int64_t w_hi = kTileCost + (d->C_max * g + kBlk - 1) / kBlk + kUnitCost;
+  const int64_t w_hi = kTileCost + (d->C_max * g + kBlk - 1) / kBlk + kExtraMax;
   if ((int64_t)kMaxSeqs * ((d->S_max + tile - 1) / tile) * w_hi >= ((int64_t)1 << 31)) return SPECMOE_ERR_SHAPE;
   return SPECMOE_OK;
 }
