@@ -269,7 +269,7 @@ int specmoe_verify_attn_paged(const void* q, const void* k_pages, const void* v_
  * sequences, at offsets that depend only on Hkv -- followed by the partial
  * results of pieces (two slots per workgroup).  The zeroed region must be
  * zero before the first call; every call that completes leaves the counters
- * zero again (the piece that merges a unit resets the unit's counter), so a
+ * zero again (the workgroup that merges a unit resets its counter), so a
  * workspace initialised once by specmoe_verify_attn_workspace_init can be
  * reused for any number of calls with the same Hkv, any B, lengths and
  * grid_blocks, as long as it is large enough for them. */

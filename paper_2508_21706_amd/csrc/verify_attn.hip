@@ -129,7 +129,7 @@ struct Params {
   float* lse;
   int* status;      // sticky flags of the workspace: kGaveUp once an in-kernel wait gave up
   int spin_limit;   // polls before an in-kernel wait gives up
-  int* counters;    // [B*Hkv] pieces arrived per unit, zero between calls
+  int* counters;    // [B*Hkv] pieces arrived per unit (| kClaimed once a merge is claimed), zero between calls
   float* ws_o;      // [2P][Rcap][D] normalised partial outputs
   float* ws_lse;    // [2P][Rcap] partial log-sum-exp
   int ws_o_bytes, ws_lse_bytes;
@@ -192,6 +192,7 @@ struct Cfg {
 // limit of 0 the counter is checked once.
 constexpr int kSpinLimit = 1 << 21;
 constexpr int kGaveUp = 1;   // status-word bit: an in-kernel wait gave up
+constexpr int kClaimed = 1 << 30;   // unit counter bit: a holder has claimed the unit's merge
 __device__ __forceinline__ bool wait_count(int* c, int target, int limit) {
   for (int spin = 0;; ++spin) {
     if (__builtin_amdgcn_readfirstlane(__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP)) >= target) {
@@ -968,9 +969,9 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   int n_pub = 0;
   // The consumer wave that counts piece k on its unit's arrival counter sets
   // bit k of counted and keeps the counter's previous value in cnt[k] (lane
-  // 0); the last piece to arrive merges the unit after the loop.  (Reading
-  // the counter back after the loop instead costs one more round trip at the
-  // end of the range, which measured slower.)
+  // 0); with HOLD the last piece to arrive merges the unit after the loop.
+  // (Reading the counter back after the loop instead costs one more round
+  // trip at the end of the range, which measured slower there.)
   int counted = 0;
   int cnt[2] = {0, 0};
   int ncb = 0;   // consumer barriers passed
@@ -1474,18 +1475,36 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     if (v + 1 < count) advance(cur, v);
   }
 
-  // ---- the last piece of a unit merges it, now that this workgroup's tiles
-  // are done.  The wave that counted piece k sets its flag (sh_flag starts
-  // at 0: no merge here; else 1 + the entry of sh_share for the unit); that
-  // wave arrived last on the piece's LDS counter, after wave 0 had written
-  // sh_share.
+  // ---- merges of cut units, now that this workgroup's tiles are done.  The
+  // wave that counted piece k sets its flag (sh_flag starts at 0: no merge
+  // here; else 1 + the entry of sh_share for the unit); that wave arrived
+  // last on the piece's LDS counter, after wave 0 had written sh_share.
+  // With HOLD the pieces are counted at the ends of their ranges and the
+  // last piece to arrive merges its unit.  Otherwise every piece is counted
+  // early in its range, and the unit is merged by the first of its holders
+  // to finish its own tiles once all pieces have arrived: it claims the unit
+  // by switching the counter from np to np | kClaimed, a compare-and-swap
+  // that fails while pieces are missing (a later holder then succeeds), once
+  // the unit is claimed, and after its merge has reset the counter to 0.
+  // (The last piece to arrive was often the last range to finish, whose
+  // merges then ended the launch.)
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     if ((counted >> k) & 1) {
       const Pub& q = k == 0 ? pub0 : pub1;
       const int e = q.unit == sh_share[0][0] ? 0 : 1;
       const int np = sh_share[e][2] - sh_share[e][1] + 1;   // pieces of the unit
-      if (lane == 0) sh_flag[k] = cnt[k] + 1 == np ? 1 + e : 0;
+      if (lane == 0) {
+        bool mine;
+        if constexpr (HOLD) {
+          mine = cnt[k] + 1 == np;
+        } else {
+          int expected = np;
+          mine = __hip_atomic_compare_exchange_strong(p.counters + q.unit, &expected, np | kClaimed, __ATOMIC_RELAXED,
+                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        sh_flag[k] = mine ? 1 + e : 0;
+      }
     }
   }
   cbar();
