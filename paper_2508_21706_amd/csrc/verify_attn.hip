@@ -537,6 +537,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   int* const cpref = HOLD ? reinterpret_cast<int*>(piece_lds) : cpref_own;
   __shared__ float mst[kConsumers][2][kBlk];   // key-split merge: max and sum of each wave's rows
   __shared__ int sh_flag[2];              // "this piece completed its unit", for the two pieces
+  __shared__ int sh_direct;               // (HOLD) the next range's piece of the last unit has arrived
   __shared__ int sh_share[2][4];          // unit, qf, ql, slot_first of the units of tiles g0 and g1 - 1
   __shared__ int full_cnt[kStages];       // producer waves whose loads of the stage's tile have landed
   __shared__ int empty_cnt[kStages];      // consumer waves done with the stage's tile
@@ -1070,11 +1071,18 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   bool pend = false, pend_whole = false, pend_ok = false;
   int pend_row = 0;
   float pend_inv = 0.f, pend_lse = 0.f;
+  // (HOLD) When the range's last segment is the head of a unit cut with the
+  // next range only, its piece stays in registers (pend_direct) and is merged
+  // after the loop with the next range's piece if that has arrived by then
+  // (the unit's counter, read at the last tile into probe by wave 0, lane
+  // 0); else it is stored and counted then, as the loop would have.
+  bool pend_direct = false;
+  int pend_k = 0, probe = 0;
 
   for (int v = 0;; ++v) {
     // (a held piece is stored at iteration count - 1, so no piece is held here)
     if (v >= count && pub0.state != 0 && pub1.state != 0 && !pend) break;
-    if (pend && pend_ok) {
+    if (pend && pend_ok && !pend_direct) {
       const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
       const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
       if (pend_whole) {
@@ -1107,7 +1115,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
                                                    (pend_row * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent);
       }
     }
-    if (pend) {
+    if (pend && !pend_direct) {
       // the next tile starts a new segment
 #pragma unroll
       for (int db = 0; db < C::kDB; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -1465,7 +1473,22 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         if (hold) {
           pend_ok = false;   // written to LDS by the key-split merge above
           q.state = 3;
-          q.v = count - 1;   // the iteration that stores it
+          // the iteration that stores it: three quarters into the range, so
+          // that it has arrived when the previous range, which merges the
+          // unit, ends (a store that early costs the stream less than that
+          // merge's wait; both halves of the range's tiles measured slower)
+          q.v = min(count - 1, max(v + 1, (3 * count) / 4));
+        }
+        if constexpr (HOLD) {
+          // (every consumer wave has passed the key-split merge's barriers,
+          // so sh_share is written)
+          if (v == count - 1 && sh_share[1][0] == q.unit && sh_share[1][1] == pid && sh_share[1][2] == pid + 1) {
+            pend_direct = true;
+            pend_k = n_pub;
+            q.state = 2;   // not published in the loop
+            if (wc == 0 && lane == 0)
+              probe = __hip_atomic_load(p.counters + q.unit, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
         }
         if (n_pub == 0) pub0 = q;
         else pub1 = q;
@@ -1473,6 +1496,88 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       }
     }
     if (v + 1 < count) advance(cur, v);
+  }
+
+  // ---- (HOLD) the head piece kept in registers: merged with the next
+  // range's piece (its first segment, slot 2 (pid + 1)) into the final rows
+  // when that piece had arrived at the last tile, else stored and counted.
+  if constexpr (HOLD) {
+    if (pend_direct) {
+      const int u = sh_share[1][0], ql = sh_share[1][2];
+      if (wc == 0 && lane == 0) sh_direct = probe == 1 ? 1 : 0;   // np - 1 pieces
+      cbar();
+      const __amdgpu_buffer_rsrc_t ws_o_rsrc =
+          __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
+      const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
+          __builtin_amdgcn_make_buffer_rsrc(p.ws_lse, 0, p.ws_lse_bytes, kBufferFormat);
+      const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
+      const int d_lo = kslot * s_db, d_hi = d_lo + s_db;   // this wave's d blocks
+      if (sh_direct) {
+        if (pend_ok) {
+          const int srow = 2 * ql * p.Rcap + row;
+          const float lp = __builtin_bit_cast(
+              float, __builtin_amdgcn_raw_buffer_load_b32(ws_lse_rsrc, srow * 4, 0, kDeviceCoherent));
+          f32x4 xp[C::kDB];
+#pragma unroll
+          for (int db = 0; db < C::kDB; ++db)
+            if (db >= d_lo && db < d_hi)
+              xp[db] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                     ws_o_rsrc, (srow * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent));
+          // this range's piece, then the next range's, as the merge of
+          // pieces takes them
+          float m = -INFINITY, z = 0.f, wa = 0.f, wb = 0.f;
+          if (pend_lse != -INFINITY) {
+            m = pend_lse;
+            z = 1.f;
+            wa = 1.f;
+          }
+          if (lp != -INFINITY) {
+            const float nm = fmaxf(m, lp);
+            const float a = expf(m - nm);
+            const float w = expf(lp - nm);
+            z = z * a + w;
+            wa *= a;
+            wb = w;
+            m = nm;
+          }
+          const float inv_z = z > 0.f ? 1.f / z : 0.f;
+          // (cur is still the last tile's cursor)
+          const int pend_orow = (cur.b * p.C_max + tok) * p.Hq + cur.kvh * g + row - tok * g;
+          float* dst = p.out + (size_t)pend_orow * D;
+#pragma unroll
+          for (int db = 0; db < C::kDB; ++db)
+            if (db >= d_lo && db < d_hi)
+              *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = (o[db] * pend_inv * wa + wb * xp[db]) * inv_z;
+          if (kslot == 0 && lg == 0) p.lse[pend_orow] = z > 0.f ? m + logf(z) : -INFINITY;
+        }
+        if (ctid == 0) __hip_atomic_store(p.counters + u, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      } else {
+        if (pend_ok) {
+          if (kslot == 0 && lg == 0)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, pend_lse), ws_lse_rsrc, pend_row * 4, 0,
+                                                  kDeviceCoherent);
+#pragma unroll
+          for (int db = 0; db < C::kDB; ++db)
+            if (db >= d_lo && db < d_hi)
+              __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(i32x4, o[db] * pend_inv), ws_o_rsrc,
+                                                     (pend_row * D + 16 * db + 4 * lg) * 4, 0, kDeviceCoherent);
+        }
+        // counted as in the loop: after every wave's stores, by the last wave
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        int last = 0;
+        if (lane == 0)
+          last = __hip_atomic_fetch_add(&pub_arrive[pend_k], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) ==
+                 kConsumers - 1;
+        if (uniform(last)) {
+          if (lane == 0) {
+            const int c = __hip_atomic_fetch_add(p.counters + u, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (pend_k == 0) cnt[0] = c;   // (constant indices keep cnt in registers)
+            else cnt[1] = c;
+          }
+          counted |= 1 << pend_k;
+        }
+      }
+    }
   }
 
   // ---- merges of cut units, now that this workgroup's tiles are done.  The
