@@ -516,10 +516,10 @@ __device__ __forceinline__ void merge_units(const Params& p, const uint32_t* seq
 // TREE: the draft region obeys per-token draft-mask words instead of the
 // chain mask.  PAGED: the KV cache is a pool of pages found through a block
 // table.  MODE kModeHold (launches whose units have at most two 16-row
-// blocks): each range is streamed in order, and the piece of its first
-// segment is held in LDS until the range's last tile.  MODE kModeNt: results
-// are stored with the non-temporal policy (launches with many units per
-// workgroup and a large output).
+// blocks): the piece of a range's first segment is held in LDS until three
+// quarters into the range.  MODE kModeNt: results are stored with the
+// non-temporal policy (launches with many units per workgroup and a large
+// output).
 template <int ELT, int D, bool TREE, bool PAGED, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   constexpr bool HOLD = MODE == kModeHold;
@@ -623,9 +623,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // ---- prologue, by wave 0 alone while the other waves wait at one
   // barrier (every wave doing it was issue-bound): the lengths, tile and cost
   // prefix sums into LDS, then this workgroup's range [g0, g1) and its first
-  // tile.  Lane l owns the contiguous sequences [l per, (l + 1) per).  The
-  // range is streamed in order, except that without HOLD a cut unit at its
-  // end is streamed first (below).
+  // tile.  Lane l owns the contiguous sequences [l per, (l + 1) per).  Every
+  // range is streamed in order.
   __shared__ int sh_sched[12];
   if (wave == 0) {
     const int per = (B + 63) / 64;
@@ -709,25 +708,12 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       cu.j = off - cu.kvh * n;
       return cu;
     };
-    int g0 = 0, g1 = 0, nL = 0, s_last = 0;
+    int g0 = 0, g1 = 0;
     Cursor first = {0, 0, 0, 0u};
     if (pid < sc.Pe) {
       g0 = range_begin_w0(pid);
       g1 = range_begin_w0(pid + 1);
-      if constexpr (HOLD) {
-        first = locate_w0(g0);
-      } else {
-        // If the range's last tile lies in a unit that starts inside the
-        // range and continues past it, that last segment [s_last, g1) is
-        // streamed first, then [g0, s_last): its piece is then stored early
-        // and merged after the loop without holding the launch's end up.
-        first = locate_w0(g1 - 1);
-        s_last = g1 - 1 - first.j;
-        const bool rotated = s_last > g0 && first.j < seq_tiles<C>(first.s) - 1;
-        nL = rotated ? g1 - s_last : 0;    // tiles of the rotated segment
-        if (rotated) first.j = 0;
-        else first = locate_w0(g0);
-      }
+      first = locate_w0(g0);
     }
     if (lane == 0) {
       sh_sched[0] = total;
@@ -736,8 +722,6 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       sh_sched[10] = sc.uni ? 1 : 0;
       sh_sched[2] = g0;
       sh_sched[3] = g1;
-      sh_sched[4] = nL;
-      sh_sched[5] = s_last;
       sh_sched[6] = first.b;
       sh_sched[7] = first.kvh;
       sh_sched[8] = first.j;
@@ -756,16 +740,12 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   }
   const int g0 = uniform(sh_sched[2]);
   const int g1 = uniform(sh_sched[3]);
-  const int nL = uniform(sh_sched[4]);
-  const int s_last = uniform(sh_sched[5]);
   const int count = g1 - g0;
   Cursor first;
   first.b = uniform(sh_sched[6]);
   first.kvh = uniform(sh_sched[7]);
   first.j = uniform(sh_sched[8]);
   first.s = uniform(seqs[first.b]);
-  // global index of the tile at position v of the workgroup's order
-  auto tile_at = [&](int v) { return v < nL ? s_last + v : g0 + (v - nL); };
   // the first tile of unit (b, kvh) after cursor cu's unit
   auto next_unit = [&](Cursor& cu) {
     cu.j = 0;
@@ -777,20 +757,16 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       cu.s = uniform(seqs[cu.b]);
     }
   };
-  // the tile after position v (in the workgroup's order) of cursor cu
-  auto advance = [&](Cursor& cu, int v) {
-    if (v + 1 == nL) cu = locate(g0);   // end of the rotated segment
-    else if (++cu.j == seq_tiles<C>(cu.s)) next_unit(cu);
+  // the tile after cursor cu
+  auto advance = [&](Cursor& cu) {
+    if (++cu.j == seq_tiles<C>(cu.s)) next_unit(cu);
   };
-  // the first tile of the segment after the one cu is in (cu at position v)
+  // the first tile of the segment after the one cu is in (cu at position v
+  // of the range): its position v_next and cursor
   auto next_segment = [&](const Cursor& cu, int v, int& v_next) {
-    const int part_end = v < nL ? nL : count;
-    v_next = min(v + seq_tiles<C>(cu.s) - cu.j, part_end);
+    v_next = min(v + seq_tiles<C>(cu.s) - cu.j, count);
     Cursor nx = cu;
-    if (v_next < count) {
-      if (v_next == nL) nx = locate(g0);
-      else next_unit(nx);
-    }
+    if (v_next < count) next_unit(nx);
     return nx;
   };
 
@@ -948,9 +924,11 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // segment).  Two tiles after a piece's stores, each consumer wave waits for
   // its own stores (a wait no tile load shares) and arrives on an LDS
   // counter; the last of the eight counts the piece on its unit's arrival
-  // counter.  The counts are read back after the loop,
-  // where the last piece of a unit merges it.  The loop runs idle iterations
-  // after the last tile until every piece is counted.
+  // counter.  The counts are read back after the loop, where the unit's
+  // merge is decided.  The loop runs idle iterations after the last tile
+  // until every piece is counted.  The last segment's piece of a unit that
+  // starts in the range is not published in the loop: it stays in registers
+  // (pend_direct) for the merge after the loop.
   struct Pub {
     int state;   // 0 stored, 1 counted, 2 no piece, 3 held in LDS
     int unit, v, rows;
@@ -998,7 +976,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int grp = wave >> 1;
     Cursor cu = first;
     int v = grp;
-    if (grp == 1 && count > 1) advance(cu, 0);
+    if (grp == 1 && count > 1) advance(cu);
     int pg = 0;   // (paged) the pages of the pair's next tile
     if constexpr (PAGED)
       if (v < count) pg = load_pages(cu);
@@ -1009,8 +987,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       if constexpr (PAGED) {
         // the next tile's table entries ride the wait for this tile's loads
         if (v + 2 < count) {
-          advance(cu, v);
-          advance(cu, v + 1);
+          advance(cu);
+          advance(cu);
           pg = load_pages(cu);
         }
       }
@@ -1018,8 +996,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
       signal_count(&full_cnt[grp]);
       if constexpr (!PAGED) {
         if (v + 2 < count) {
-          advance(cu, v);
-          advance(cu, v + 1);
+          advance(cu);
+          advance(cu);
         }
       }
     }
@@ -1071,11 +1049,12 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   bool pend = false, pend_whole = false, pend_ok = false;
   int pend_row = 0;
   float pend_inv = 0.f, pend_lse = 0.f;
-  // (HOLD) When the range's last segment is the head of a unit cut with the
-  // next range only, its piece stays in registers (pend_direct) and is merged
-  // after the loop with the next range's piece if that has arrived by then
-  // (the unit's counter, read at the last tile into probe by wave 0, lane
-  // 0); else it is stored and counted then, as the loop would have.
+  // When the range's last segment starts a unit that continues into later
+  // ranges, its piece stays in registers (pend_direct) and, if the unit has
+  // just one more piece (the next range's first segment) and that piece has
+  // arrived (the unit's counter, read at the last tile into probe by wave 0,
+  // lane 0), is merged with it after the loop into the final rows; else it
+  // is stored and counted then, as the loop would have.
   bool pend_direct = false;
   int pend_k = 0, probe = 0;
 
@@ -1173,9 +1152,9 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
     const int b = cur.b, kvh = cur.kvh, j = cur.j;
     const uint32_t s = cur.s;
     const int n = seq_tiles<C>(s);
-    const int gt = tile_at(v);
-    const bool seg_first = v == 0 || v == nL || j == 0;
-    const bool seg_last = v == count - 1 || v + 1 == nL || j == n - 1;
+    const int gt = g0 + v;
+    const bool seg_first = v == 0 || j == 0;
+    const bool seg_last = v == count - 1 || j == n - 1;
     if (seg_first) {
       roles(cur);
       m_run = -INFINITY;
@@ -1479,10 +1458,8 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
           // merge's wait; both halves of the range's tiles measured slower)
           q.v = min(count - 1, max(v + 1, (3 * count) / 4));
         }
-        if constexpr (HOLD) {
-          // (every consumer wave has passed the key-split merge's barriers,
-          // so sh_share is written)
-          if (v == count - 1 && sh_share[1][0] == q.unit && sh_share[1][1] == pid && sh_share[1][2] == pid + 1) {
+        {
+          if (v == count - 1 && unit_first >= g0) {
             pend_direct = true;
             pend_k = n_pub;
             q.state = 2;   // not published in the loop
@@ -1495,17 +1472,22 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
         ++n_pub;
       }
     }
-    if (v + 1 < count) advance(cur, v);
+    if (v + 1 < count) advance(cur);
   }
 
-  // ---- (HOLD) the head piece kept in registers: merged with the next
+  // ---- the last segment's piece kept in registers: merged with the next
   // range's piece (its first segment, slot 2 (pid + 1)) into the final rows
-  // when that piece had arrived at the last tile, else stored and counted.
-  if constexpr (HOLD) {
+  // when that was the unit's only other piece and it had arrived at the last
+  // tile, else stored and counted.  (Merging there saves the piece's store,
+  // its count and a read back at the end of the launch, when nothing else
+  // hides them: the next range publishes its piece early.)
+  {
     if (pend_direct) {
-      const int u = sh_share[1][0], ql = sh_share[1][2];
-      if (wc == 0 && lane == 0) sh_direct = probe == 1 ? 1 : 0;   // np - 1 pieces
+      // two pieces, the other one arrived (wave 0 wrote sh_share itself;
+      // the other waves read it after the barrier)
+      if (wc == 0 && lane == 0) sh_direct = sh_share[1][2] == pid + 1 && probe == 1 ? 1 : 0;
       cbar();
+      const int u = sh_share[1][0], ql = sh_share[1][2];
       const __amdgpu_buffer_rsrc_t ws_o_rsrc =
           __builtin_amdgcn_make_buffer_rsrc(p.ws_o, 0, p.ws_o_bytes, kBufferFormat);
       const __amdgpu_buffer_rsrc_t ws_lse_rsrc =
@@ -1547,8 +1529,16 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
 #pragma unroll
           for (int db = 0; db < C::kDB; ++db)
             if (db >= d_lo && db < d_hi)
-              *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = (o[db] * pend_inv * wa + wb * xp[db]) * inv_z;
-          if (kslot == 0 && lg == 0) p.lse[pend_orow] = z > 0.f ? m + logf(z) : -INFINITY;
+            {
+              const f32x4 res = (o[db] * pend_inv * wa + wb * xp[db]) * inv_z;
+              if constexpr (NT) __builtin_nontemporal_store(res, reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg));
+              else *reinterpret_cast<f32x4*>(dst + 16 * db + 4 * lg) = res;
+            }
+          if (kslot == 0 && lg == 0) {
+            const float res_lse = z > 0.f ? m + logf(z) : -INFINITY;
+            if constexpr (NT) __builtin_nontemporal_store(res_lse, p.lse + pend_orow);
+            else p.lse[pend_orow] = res_lse;
+          }
         }
         if (ctid == 0) __hip_atomic_store(p.counters + u, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       } else {
@@ -1584,15 +1574,14 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   // wave that counted piece k sets its flag (sh_flag starts at 0: no merge
   // here; else 1 + the entry of sh_share for the unit); that wave arrived
   // last on the piece's LDS counter, after wave 0 had written sh_share.
-  // With HOLD the pieces are counted at the ends of their ranges and the
-  // last piece to arrive merges its unit.  Otherwise every piece is counted
-  // early in its range, and the unit is merged by the first of its holders
-  // to finish its own tiles once all pieces have arrived: it claims the unit
-  // by switching the counter from np to np | kClaimed, a compare-and-swap
-  // that fails while pieces are missing (a later holder then succeeds), once
-  // the unit is claimed, and after its merge has reset the counter to 0.
-  // (The last piece to arrive was often the last range to finish, whose
-  // merges then ended the launch.)
+  // (Units merged from registers above are not counted here.)  With HOLD
+  // the last piece to arrive merges its unit.  Otherwise the unit is merged
+  // by the first of its holders to finish its own tiles once all pieces have
+  // arrived: it claims the unit by switching the counter from np to np |
+  // kClaimed, a compare-and-swap that fails while pieces are missing (a
+  // later holder then succeeds), once the unit is claimed, and after its
+  // merge has reset the counter to 0.  (The last piece to arrive was often
+  // the last range to finish, whose merges then ended the launch.)
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     if ((counted >> k) & 1) {
