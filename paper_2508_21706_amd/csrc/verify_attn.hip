@@ -1059,7 +1059,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   int pend_k = 0, probe = 0;
 
   for (int v = 0;; ++v) {
-    // (a held piece is stored at iteration count - 1, so no piece is held here)
+    // (a held piece is stored by iteration count - 1, so no piece is held here)
     if (v >= count && pub0.state != 0 && pub1.state != 0 && !pend) break;
     if (pend && pend_ok && !pend_direct) {
       const int s_db = nks <= C::kDB ? C::kDB / nks : 1;
