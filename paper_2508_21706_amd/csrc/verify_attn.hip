@@ -26,11 +26,14 @@
 //     pass or second launch is needed.  A unit cut by a range
 //     boundary is a sequence-wise KV partition whose partial results must be
 //     combined, as the paper notes for its sequence-dimension KV split
-//     (Section 5.2): each piece writes (O/l, lse) to the workspace and counts
-//     itself on an arrival counter; the last piece to arrive merges all of
-//     them with log-sum-exp weights, after its own tiles.  A workgroup streams
-//     the cut unit at the end of its range first, so both pieces of every cut
-//     unit are done early in the launch.
+//     (Section 5.2).  Ranges are streamed in order.  The piece of a range's
+//     first segment is written as (O/l, lse) to the workspace and counted on
+//     the unit's arrival counter; the piece of its last segment stays in
+//     registers, and after its tiles the range merges it with log-sum-exp
+//     weights with the next range's piece, when that is the unit's only
+//     other piece and has arrived.  Other cut units are merged from the
+//     workspace after the tiles of the last piece to arrive or of the first
+//     holder to finish.
 //   * Warp-specialised pipeline: 4 producer waves stream K/V tiles from HBM
 //     straight into LDS with direct-to-LDS loads (one wave instruction moves
 //     1 KB of contiguous cache rows); 8 consumer waves compute.  The producers
@@ -403,8 +406,8 @@ struct Cursor {
   uint32_t s;
 };
 
-// Merge every piece of up to two units: those whose last piece this
-// workgroup published, run by its consumer threads after its own tiles.  A
+// Merge every piece of up to two units: those that this workgroup merges
+// through the workspace, run by its consumer threads after its own tiles.  A
 // unit's pieces come from ranges qf..ql; range q's piece is its first
 // segment (slot 2q), except for range qf when it starts before the unit:
 // then it is qf's last segment (slot_first = 2 qf + 1).  The (row, 4 d)
@@ -537,7 +540,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
   int* const cpref = HOLD ? reinterpret_cast<int*>(piece_lds) : cpref_own;
   __shared__ float mst[kConsumers][2][kBlk];   // key-split merge: max and sum of each wave's rows
   __shared__ int sh_flag[2];              // "this piece completed its unit", for the two pieces
-  __shared__ int sh_direct;               // (HOLD) the next range's piece of the last unit has arrived
+  __shared__ int sh_direct;               // the next range's piece of the last unit had arrived at the last tile
   __shared__ int sh_share[2][4];          // unit, qf, ql, slot_first of the units of tiles g0 and g1 - 1
   __shared__ int full_cnt[kStages];       // producer waves whose loads of the stage's tile have landed
   __shared__ int empty_cnt[kStages];      // consumer waves done with the stage's tile
@@ -1455,7 +1458,7 @@ __global__ __launch_bounds__(kThreads, 1) void verify_attn_kernel(Params p) {
           // the iteration that stores it: three quarters into the range, so
           // that it has arrived when the previous range, which merges the
           // unit, ends (a store that early costs the stream less than that
-          // merge's wait; both halves of the range's tiles measured slower)
+          // merge's wait; halfway and seven eighths in measured slower)
           q.v = min(count - 1, max(v + 1, (3 * count) / 4));
         }
         {
